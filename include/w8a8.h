@@ -1,0 +1,131 @@
+/*
+ * w8a8.h -- C ABI of libw8a8.so, a fused W8A8 quantized linear for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The operation (Section 3 of "Realizing Native INT8 Compute for Diffusion
+ * Transformers on Consumer GPUs", paragraphs "The quantization recipe (reused)" and
+ * "The fused kernel"): a bf16 linear layer Y = X W^T + b, with X [M,K] (M tokens),
+ * W [N,K] (N output channels) and b [N], is replaced by
+ *   1. per-output-channel int8 weights Wq [N,K] with float32 scales sw [N]
+ *      (computed once, offline);
+ *   2. per-token dynamic int8 activations Xq [M,K] with float32 scales sx [M]
+ *      (computed on every call);
+ *   3. the exact product acc = Xq Wq^T in int32 on the int8 matrix cores, whose
+ *      epilogue dequantizes off the accumulator and adds the bias:
+ *      Y[m][n] = bf16(fmaf((float)acc[m][n], sx[m] * sw[n], b[n])).
+ *
+ * Quantization of a row v[0..K) (both W and X):
+ *   a = max_k |v[k]|, s = a / 127, q[k] = clamp(rne(v[k] * (127 / a)), -127, 127);
+ *   every division is a correctly rounded float32 division, rne is round half to even;
+ *   a row with a == 0, or with 127/a overflowing float32, gets s = 0 and q = 0.
+ *
+ * Conventions for every entry point:
+ *   - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ *   - All matrices are row-major and contiguous with K innermost: X [M,K], W [N,K],
+ *     Xq [M,K], Wq [N,K]; Y and acc are [M,N] with N innermost.
+ *   - Tensor pointers are device pointers (HIP device memory of the current device);
+ *     `stream` is a hipStream_t (NULL = the legacy default stream). All work is
+ *     enqueued on `stream`; no call synchronizes, allocates or frees memory.
+ *   - The caller owns every buffer. The library keeps no state besides its immutable
+ *     kernel and tile tables, so concurrent calls on different streams are safe when
+ *     their output and workspace buffers do not overlap.
+ *   - Arguments are validated before anything is launched; on a non-zero status
+ *     nothing was enqueued (W8A8_ERR_HIP excepted: a launch that HIP rejected).
+ *   - M == 0 or N == 0 is a valid no-op. K == 0 is valid: every code is 0, every
+ *     scale 0, and Y = b.
+ *   - Inputs must be finite; for non-finite X, W or b the results are unspecified.
+ *   - Any alignment and any K are accepted; 16-byte aligned operands with K a multiple
+ *     of 16 take the fast kernels, others a slower generic kernel with the same results.
+ */
+#ifndef W8A8_H
+#define W8A8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int w8a8_status;
+
+enum {
+    W8A8_OK = 0,
+    W8A8_ERR_NULL = 1,        /* a pointer that the sizes make necessary is NULL */
+    W8A8_ERR_SHAPE = 2,       /* a negative size, or M*K / N*K / M*N beyond 2^62 */
+    W8A8_ERR_K_OVERFLOW = 3,  /* K > W8A8_MAX_K: 127*127*K would not fit int32 */
+    W8A8_ERR_HIP = 4,         /* HIP reported an error for a launch */
+    W8A8_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query returns */
+    W8A8_ERR_ARG = 6          /* another invalid argument (e.g. unknown tile id) */
+};
+
+/* Largest K for which |acc| <= 127 * 127 * K fits int32. */
+#define W8A8_MAX_K 133144
+
+/* Per-output-channel weight quantization (step 1; offline, once per layer).
+ * w: [N,K] bf16. Out: wq [N,K] int8, w_scale [N] float32. */
+w8a8_status w8a8_quantize_weight(const uint16_t *w, int64_t N, int64_t K, int8_t *wq,
+                                 float *w_scale, void *stream);
+
+/* Per-token dynamic activation quantization (step 2; every forward).
+ * x: [M,K] bf16. Out: xq [M,K] int8, x_scale [M] float32. Same rule as above. */
+w8a8_status w8a8_quantize_act(const uint16_t *x, int64_t M, int64_t K, int8_t *xq,
+                              float *x_scale, void *stream);
+
+/* Fused int8 GEMM + dequantization epilogue (step 3): Y = bf16(fmaf((float)(Xq Wq^T),
+ * sx[m] * sw[n], b[n])). bias: [N] bf16 or NULL (no bias). y: [M,N] bf16.
+ * workspace: device scratch of at least w8a8_gemm_workspace_bytes(M,N,K) bytes (NULL
+ * allowed when that is 0); 256-byte aligned. */
+w8a8_status w8a8_gemm(const int8_t *xq, const float *x_scale, const int8_t *wq,
+                      const float *w_scale, const uint16_t *bias, uint16_t *y,
+                      int64_t M, int64_t N, int64_t K, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
+size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/* The whole quantized linear: per-token quantization of x into the workspace, then the
+ * fused GEMM (steps 2 and 3). wq / w_scale come from w8a8_quantize_weight.
+ * workspace: at least w8a8_linear_workspace_bytes(M,N,K) bytes, 256-byte aligned; it
+ * holds Xq [M,K] and sx [M] (and whatever the GEMM needs) and may be reused once the
+ * call's work on `stream` has finished. */
+w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scale,
+                        const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                        int64_t K, void *workspace, size_t workspace_bytes,
+                        void *stream);
+
+size_t w8a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/* Debug: the raw int32 accumulator acc [M,N] = Xq Wq^T, with no epilogue. It is the
+ * exactness check the paper runs against a library integer matmul (Section 5,
+ * "The kernel is exact and the GEMMs are compute-bound"). */
+w8a8_status w8a8_gemm_acc_i32(const int8_t *xq, const int8_t *wq, int32_t *acc,
+                              int64_t M, int64_t N, int64_t K, void *stream);
+
+/* Tile configurations (the per-shape table chosen offline, Section 3, "Why
+ * autotuning is load-bearing"). w8a8_select_tile returns the id the table picks for a
+ * shape; the _ex variants run a given id (-1 = the table's choice) for offline sweeps
+ * and tests. An id outside [0, w8a8_tile_count()) returns W8A8_ERR_ARG. */
+int w8a8_tile_count(void);
+const char *w8a8_tile_name(int tile_id);
+int w8a8_select_tile(int64_t M, int64_t N, int64_t K);
+
+w8a8_status w8a8_gemm_ex(const int8_t *xq, const float *x_scale, const int8_t *wq,
+                         const float *w_scale, const uint16_t *bias, uint16_t *y,
+                         int64_t M, int64_t N, int64_t K, void *workspace,
+                         size_t workspace_bytes, int tile_id, void *stream);
+
+w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *acc,
+                                 int64_t M, int64_t N, int64_t K, int tile_id,
+                                 void *stream);
+
+/* Static description of a status code. */
+const char *w8a8_status_string(w8a8_status status);
+
+/* Library version string. */
+const char *w8a8_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* W8A8_H */

@@ -1,0 +1,243 @@
+"""Fused W8A8 quantized linear for MI355X (gfx950): Python binding of libw8a8.so.
+
+The arithmetic all runs in the library's HIP kernels; this module only checks
+arguments, allocates outputs with torch and passes raw device pointers and torch's
+current HIP stream through ctypes. Entry points mirror the C ABI in include/w8a8.h:
+
+  quantize_weight(w)                 -> (wq int8 [N,K], w_scale fp32 [N])
+  quantize_act(x)                    -> (xq int8 [M,K], x_scale fp32 [M])
+  gemm(xq, x_scale, wq, w_scale, b)  -> y bf16 [M,N]
+  linear(x, wq, w_scale, b)          -> y bf16 [..., N]   (x [..., K])
+  gemm_acc_i32(xq, wq)               -> acc int32 [M,N]   (debug, no epilogue)
+
+The method is Section 3 of the paper ("The quantization recipe (reused)", "The fused
+kernel"): per-channel int8 weights, per-token dynamic int8 activations, an int8 x int8
+-> int32 product, and an epilogue that applies sx[m] * sw[n] and the bias off the
+int32 accumulator. If the library is missing, every call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
+           "tile_count", "tile_name", "select_tile", "gemm_workspace_bytes",
+           "linear_workspace_bytes", "library_path", "load_library", "W8A8Error",
+           "MAX_K", "version"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libw8a8.so")
+MAX_K = 133144
+
+_lib = None
+
+
+class W8A8Error(RuntimeError):
+    def __init__(self, func: str, status: int, msg: str):
+        super().__init__(f"{func} failed with status {status}: {msg}")
+        self.status = status
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def load_library():
+    """Load libw8a8.so (built in-tree by paper_2606_14598_amd.build). Raises if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2606_14598_amd.build` "
+            "(the W8A8 path has no fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, SZ, INT = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_int
+    sigs = {
+        "w8a8_quantize_weight": ([P, I64, I64, P, P, P], INT),
+        "w8a8_quantize_act": ([P, I64, I64, P, P, P], INT),
+        "w8a8_gemm": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
+        "w8a8_gemm_ex": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, INT, P], INT),
+        "w8a8_gemm_workspace_bytes": ([I64, I64, I64], SZ),
+        "w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
+        "w8a8_linear_workspace_bytes": ([I64, I64, I64], SZ),
+        "w8a8_gemm_acc_i32": ([P, P, P, I64, I64, I64, P], INT),
+        "w8a8_gemm_acc_i32_ex": ([P, P, P, I64, I64, I64, INT, P], INT),
+        "w8a8_tile_count": ([], INT),
+        "w8a8_tile_name": ([INT], ctypes.c_char_p),
+        "w8a8_select_tile": ([I64, I64, I64], INT),
+        "w8a8_status_string": ([INT], ctypes.c_char_p),
+        "w8a8_version": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sigs.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def _call(name: str, *args) -> None:
+    lib = load_library()
+    st = getattr(lib, name)(*args)
+    if st != 0:
+        raise W8A8Error(name, st, lib.w8a8_status_string(st).decode())
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check(t: torch.Tensor, dtype: torch.dtype, ndim: int, name: str):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D, got shape {tuple(t.shape)}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) > 1:
+        raise ValueError(f"tensors on different devices: {devs}")
+
+
+def version() -> str:
+    return load_library().w8a8_version().decode()
+
+
+def tile_count() -> int:
+    return int(load_library().w8a8_tile_count())
+
+
+def tile_name(tile_id: int) -> str:
+    r = load_library().w8a8_tile_name(tile_id)
+    if r is None:
+        raise ValueError(f"no tile {tile_id}")
+    return r.decode()
+
+
+def select_tile(M: int, N: int, K: int) -> int:
+    return int(load_library().w8a8_select_tile(M, N, K))
+
+
+def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(load_library().w8a8_gemm_workspace_bytes(M, N, K))
+
+
+def linear_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(load_library().w8a8_linear_workspace_bytes(M, N, K))
+
+
+def _quantize(fn: str, v: torch.Tensor, name: str):
+    _check(v, torch.bfloat16, 2, name)
+    R, K = v.shape
+    q = torch.empty((R, K), dtype=torch.int8, device=v.device)
+    s = torch.empty((R,), dtype=torch.float32, device=v.device)
+    with torch.cuda.device(v.device):
+        _call(fn, _ptr(v), R, K, _ptr(q), _ptr(s), _stream(v.device))
+    return q, s
+
+
+def quantize_weight(w: torch.Tensor):
+    """Per-output-channel int8 weights: w bf16 [N,K] -> (wq int8 [N,K], sw fp32 [N])."""
+    return _quantize("w8a8_quantize_weight", w, "w")
+
+
+def quantize_act(x: torch.Tensor):
+    """Per-token int8 activations: x bf16 [M,K] -> (xq int8 [M,K], sx fp32 [M])."""
+    return _quantize("w8a8_quantize_act", x, "x")
+
+
+def _workspace(nbytes: int, device, workspace):
+    if nbytes == 0:
+        return None
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError(f"workspace needs {nbytes} bytes")
+        return workspace
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def gemm(xq, x_scale, wq, w_scale, bias=None, *, tile: int = -1, out=None,
+         workspace=None):
+    """Fused int8 GEMM + epilogue: bf16(fmaf(float(xq @ wq^T), sx[m]*sw[n], b[n]))."""
+    _check(xq, torch.int8, 2, "xq")
+    _check(wq, torch.int8, 2, "wq")
+    _check(x_scale, torch.float32, 1, "x_scale")
+    _check(w_scale, torch.float32, 1, "w_scale")
+    if bias is not None:
+        _check(bias, torch.bfloat16, 1, "bias")
+    _same_device(xq, wq, x_scale, w_scale, bias)
+    M, K = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != K or x_scale.shape[0] != M or w_scale.shape[0] != N or (
+            bias is not None and bias.shape[0] != N):
+        raise ValueError("shape mismatch")
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
+                                                device=xq.device)
+    _check(y, torch.bfloat16, 2, "out")
+    ws = _workspace(gemm_workspace_bytes(M, N, K), xq.device, workspace)
+    nws = 0 if ws is None else ws.numel() * ws.element_size()
+    with torch.cuda.device(xq.device):
+        _call("w8a8_gemm_ex", _ptr(xq), _ptr(x_scale), _ptr(wq), _ptr(w_scale), _ptr(bias),
+              _ptr(y), M, N, K, _ptr(ws), nws, int(tile), _stream(xq.device))
+    return y
+
+
+def linear(x, wq, w_scale, bias=None, *, out=None, workspace=None):
+    """The whole W8A8 linear: x bf16 [..., K] -> y bf16 [..., N] (per-token
+    quantization of x, int8 GEMM, fused dequantization + bias)."""
+    if not isinstance(x, torch.Tensor) or x.dtype != torch.bfloat16:
+        raise TypeError("x must be a bf16 torch.Tensor")
+    lead = x.shape[:-1]
+    K = x.shape[-1]
+    x2 = x.reshape(lead.numel(), K)
+    _check(x2, torch.bfloat16, 2, "x")
+    _check(wq, torch.int8, 2, "wq")
+    _check(w_scale, torch.float32, 1, "w_scale")
+    if bias is not None:
+        _check(bias, torch.bfloat16, 1, "bias")
+    _same_device(x2, wq, w_scale, bias)
+    M = x2.shape[0]
+    N = wq.shape[0]
+    if wq.shape[1] != K or w_scale.shape[0] != N or (bias is not None and bias.shape[0] != N):
+        raise ValueError("shape mismatch")
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
+                                                device=x.device)
+    if M == 0 or N == 0:
+        return y.reshape(*lead, N)
+    ws = _workspace(linear_workspace_bytes(M, N, K), x.device, workspace)
+    with torch.cuda.device(x.device):
+        _call("w8a8_linear", _ptr(x2), _ptr(wq), _ptr(w_scale), _ptr(bias), _ptr(y), M, N, K,
+              _ptr(ws), ws.numel() * ws.element_size(), _stream(x.device))
+    return y.reshape(*lead, N)
+
+
+def gemm_acc_i32(xq, wq, *, tile: int = -1, out=None):
+    """Debug: the raw int32 accumulator xq @ wq^T (no epilogue)."""
+    _check(xq, torch.int8, 2, "xq")
+    _check(wq, torch.int8, 2, "wq")
+    _same_device(xq, wq)
+    M, K = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != K:
+        raise ValueError("shape mismatch")
+    acc = out if out is not None else torch.empty((M, N), dtype=torch.int32,
+                                                  device=xq.device)
+    _check(acc, torch.int32, 2, "out")
+    with torch.cuda.device(xq.device):
+        _call("w8a8_gemm_acc_i32_ex", _ptr(xq), _ptr(wq), _ptr(acc), M, N, K, int(tile),
+              _stream(xq.device))
+    return acc

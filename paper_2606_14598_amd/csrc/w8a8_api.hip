@@ -1,0 +1,212 @@
+// C ABI of libw8a8.so: argument validation, tile selection and launches on the
+// caller's stream. Nothing here allocates, frees or synchronizes.
+#include "../../include/w8a8.h"
+#include "w8a8_internal.hpp"
+
+namespace {
+
+using namespace w8a8;
+
+constexpr int64_t kMaxElems = int64_t(1) << 62;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool product_ok(int64_t a, int64_t b) { return a == 0 || b <= kMaxElems / a; }
+
+hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+w8a8_status from_hip(hipError_t e) { return e == hipSuccess ? W8A8_OK : W8A8_ERR_HIP; }
+
+bool aligned16(const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+
+w8a8_status check_quant(const void *v, int64_t rows, int64_t K, const void *q,
+                        const void *scale) {
+    if (rows < 0 || K < 0 || !product_ok(rows, K))
+        return W8A8_ERR_SHAPE;
+    if (rows > 0 && !scale)
+        return W8A8_ERR_NULL;
+    if (rows > 0 && K > 0 && (!v || !q))
+        return W8A8_ERR_NULL;
+    return W8A8_OK;
+}
+
+w8a8_status check_gemm(const int8_t *xq, const int8_t *wq, const void *out, int64_t M,
+                       int64_t N, int64_t K) {
+    if (M < 0 || N < 0 || K < 0 || !product_ok(M, K) || !product_ok(N, K) ||
+        !product_ok(M, N))
+        return W8A8_ERR_SHAPE;
+    if (K > W8A8_MAX_K)
+        return W8A8_ERR_K_OVERFLOW;
+    if (M == 0 || N == 0)
+        return W8A8_OK;
+    if (!out)
+        return W8A8_ERR_NULL;
+    if (K > 0 && (!xq || !wq))
+        return W8A8_ERR_NULL;
+    // Tile offsets inside one workgroup's panel are 32-bit (TN * K bytes < 2^31).
+    return W8A8_OK;
+}
+
+w8a8_status run_gemm(const int8_t *xq, const float *sx, const int8_t *wq, const float *sw,
+                     const uint16_t *bias, void *out, Epilogue epi, int64_t M, int64_t N,
+                     int64_t K, void *ws, size_t ws_bytes, int tile_id, hipStream_t s) {
+    if (tile_id < -1 || tile_id >= tile_count())
+        return W8A8_ERR_ARG;
+    if (M == 0 || N == 0)
+        return W8A8_OK;
+    const int id = tile_id >= 0 ? tile_id : select_tile(M, N, K);
+    const size_t need = tile_workspace_bytes(id, M, N, K);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+        return W8A8_ERR_WORKSPACE;
+    GemmArgs a;
+    a.xq = xq;
+    a.wq = wq;
+    a.sx = sx;
+    a.sw = sw;
+    a.bias = bias;
+    a.out = out;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    const bool vec = (K % 16 == 0) && aligned16(xq) && aligned16(wq);
+    return from_hip(launch_gemm(id, epi, vec, a, ws, ws_bytes, s));
+}
+
+}  // namespace
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+w8a8_status w8a8_quantize_weight(const uint16_t *w, int64_t N, int64_t K, int8_t *wq,
+                                 float *w_scale, void *stream) {
+    const w8a8_status st = check_quant(w, N, K, wq, w_scale);
+    if (st != W8A8_OK)
+        return st;
+    return from_hip(launch_quant_rows(w, N, K, wq, w_scale, as_stream(stream)));
+}
+
+w8a8_status w8a8_quantize_act(const uint16_t *x, int64_t M, int64_t K, int8_t *xq,
+                              float *x_scale, void *stream) {
+    const w8a8_status st = check_quant(x, M, K, xq, x_scale);
+    if (st != W8A8_OK)
+        return st;
+    return from_hip(launch_quant_rows(x, M, K, xq, x_scale, as_stream(stream)));
+}
+
+size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K < 0 || K > W8A8_MAX_K)
+        return 0;
+    return tile_workspace_bytes(select_tile(M, N, K), M, N, K);
+}
+
+w8a8_status w8a8_gemm_ex(const int8_t *xq, const float *x_scale, const int8_t *wq,
+                         const float *w_scale, const uint16_t *bias, uint16_t *y,
+                         int64_t M, int64_t N, int64_t K, void *workspace,
+                         size_t workspace_bytes, int tile_id, void *stream) {
+    w8a8_status st = check_gemm(xq, wq, y, M, N, K);
+    if (st != W8A8_OK)
+        return st;
+    if (M > 0 && N > 0 && (!x_scale || !w_scale))
+        return W8A8_ERR_NULL;
+    return run_gemm(xq, x_scale, wq, w_scale, bias, y, EPI_BF16, M, N, K, workspace,
+                    workspace_bytes, tile_id, as_stream(stream));
+}
+
+w8a8_status w8a8_gemm(const int8_t *xq, const float *x_scale, const int8_t *wq,
+                      const float *w_scale, const uint16_t *bias, uint16_t *y,
+                      int64_t M, int64_t N, int64_t K, void *workspace,
+                      size_t workspace_bytes, void *stream) {
+    return w8a8_gemm_ex(xq, x_scale, wq, w_scale, bias, y, M, N, K, workspace,
+                        workspace_bytes, -1, stream);
+}
+
+size_t w8a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N < 0 || K < 0 || !product_ok(M, K))
+        return 0;
+    return align_up((size_t)(M * K)) + align_up((size_t)M * sizeof(float)) +
+           w8a8_gemm_workspace_bytes(M, N, K);
+}
+
+w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scale,
+                        const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                        int64_t K, void *workspace, size_t workspace_bytes,
+                        void *stream) {
+    if (M < 0 || N < 0 || K < 0 || !product_ok(M, K) || !product_ok(N, K) ||
+        !product_ok(M, N))
+        return W8A8_ERR_SHAPE;
+    if (K > W8A8_MAX_K)
+        return W8A8_ERR_K_OVERFLOW;
+    if (M == 0 || N == 0)
+        return W8A8_OK;
+    if (!y || !w_scale || (K > 0 && (!x || !wq)))
+        return W8A8_ERR_NULL;
+    const size_t need = w8a8_linear_workspace_bytes(M, N, K);
+    if (!workspace || workspace_bytes < need)
+        return W8A8_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+        return W8A8_ERR_WORKSPACE;
+    int8_t *xq = static_cast<int8_t *>(workspace);
+    float *sx = reinterpret_cast<float *>(static_cast<char *>(workspace) +
+                                          align_up((size_t)(M * K)));
+    char *gws = reinterpret_cast<char *>(sx) + align_up((size_t)M * sizeof(float));
+    hipStream_t s = as_stream(stream);
+    hipError_t e = launch_quant_rows(x, M, K, xq, sx, s);
+    if (e != hipSuccess)
+        return W8A8_ERR_HIP;
+    return run_gemm(xq, sx, wq, w_scale, bias, y, EPI_BF16, M, N, K, gws,
+                    workspace_bytes - (size_t)(gws - static_cast<char *>(workspace)), -1, s);
+}
+
+w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *acc,
+                                 int64_t M, int64_t N, int64_t K, int tile_id,
+                                 void *stream) {
+    const w8a8_status st = check_gemm(xq, wq, acc, M, N, K);
+    if (st != W8A8_OK)
+        return st;
+    if (tile_id < -1 || tile_id >= tile_count())
+        return W8A8_ERR_ARG;
+    if (M == 0 || N == 0)
+        return W8A8_OK;
+    const int id = tile_id >= 0 ? tile_id : select_tile(M, N, K);
+    if (tile_workspace_bytes(id, M, N, K) > 0)
+        return W8A8_ERR_ARG;
+    return run_gemm(xq, nullptr, wq, nullptr, nullptr, acc, EPI_I32, M, N, K, nullptr, 0,
+                    id, as_stream(stream));
+}
+
+w8a8_status w8a8_gemm_acc_i32(const int8_t *xq, const int8_t *wq, int32_t *acc,
+                              int64_t M, int64_t N, int64_t K, void *stream) {
+    return w8a8_gemm_acc_i32_ex(xq, wq, acc, M, N, K, -1, stream);
+}
+
+int w8a8_tile_count(void) { return tile_count(); }
+
+const char *w8a8_tile_name(int tile_id) {
+    const TileInfo *t = tile_info(tile_id);
+    return t ? t->name : nullptr;
+}
+
+int w8a8_select_tile(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K < 0)
+        return -1;
+    return select_tile(M, N, K);
+}
+
+const char *w8a8_status_string(w8a8_status status) {
+    switch (status) {
+    case W8A8_OK: return "ok";
+    case W8A8_ERR_NULL: return "a required pointer is NULL";
+    case W8A8_ERR_SHAPE: return "invalid shape (negative size or element count overflow)";
+    case W8A8_ERR_K_OVERFLOW: return "K too large: 127*127*K does not fit int32";
+    case W8A8_ERR_HIP: return "HIP launch error";
+    case W8A8_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case W8A8_ERR_ARG: return "invalid argument";
+    default: return "unknown status";
+    }
+}
+
+const char *w8a8_version(void) { return "w8a8-gfx950 0.1.0"; }
+
+}  // extern "C"
+#pragma GCC visibility pop

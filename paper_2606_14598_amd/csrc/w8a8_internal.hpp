@@ -1,0 +1,46 @@
+// Internal declarations shared by the HIP translation units of libw8a8.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace w8a8 {
+
+// ---------------------------------------------------------------- quantizer
+// Launches the per-row absmax quantizer over a [rows, K] bf16 matrix on `stream`.
+// Returns hipSuccess or the launch error.
+hipError_t launch_quant_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
+                             float *scale, hipStream_t stream);
+
+// ---------------------------------------------------------------- GEMM
+enum Epilogue : int { EPI_BF16 = 0, EPI_I32 = 1 };
+
+struct GemmArgs {
+    const int8_t *xq;       // [M,K]
+    const int8_t *wq;       // [N,K]
+    const float *sx;        // [M]   (EPI_BF16)
+    const float *sw;        // [N]   (EPI_BF16)
+    const uint16_t *bias;   // [N] or nullptr
+    void *out;              // [M,N] bf16 or int32
+    int64_t M, N, K;
+};
+
+struct TileInfo {
+    const char *name;
+    int tm, tn, bk;      // workgroup tile (tokens x channels x K step)
+    int threads;         // workgroup size
+    int lds_bytes;       // static LDS per workgroup
+};
+
+int tile_count();
+const TileInfo *tile_info(int id);
+// Table lookup of the tile id for a shape (offline-chosen, with a fallback rule).
+int select_tile(int64_t M, int64_t N, int64_t K);
+// Extra device scratch a tile needs for a shape (0 for the data-parallel tiles).
+size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K);
+// Launch tile `id` with epilogue `epi`; `vec` selects the 16-byte-aligned load path.
+hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,
+                       size_t ws_bytes, hipStream_t stream);
+
+}  // namespace w8a8

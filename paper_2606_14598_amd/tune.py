@@ -1,0 +1,104 @@
+"""Offline tile sweep: time every GEMM tile on each workload shape and write the
+per-shape table (tile_table.inc) the library compiles in.
+
+The paper tunes its kernel per (M, N, K) with an autotuner over 36 configurations at
+first call (Section 3, "Why autotuning is load-bearing"); here the search runs once,
+offline, on the target GPU, and its result is a constant table in the library.
+
+Usage (on an MI355X): python -m paper_2606_14598_amd.tune --out tile_table.inc [--json r.json]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import paper_2606_14598_amd as w8a8  # noqa: E402
+import synth_inputs as si  # noqa: E402
+
+HEADER = """// Offline-chosen GEMM tile per shape: {M lower bound, M upper bound, N, K, tile id}.
+// Written by paper_2606_14598_amd/tune.py from a timed sweep of every tile on MI355X;
+// shapes not listed use the fallback rule in gemm_i8.hip.
+"""
+
+
+def time_ms(fn, iters=20, warmup=3):
+    for _ in range(warmup):
+        fn()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(iters):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / iters
+
+
+def shapes():
+    seen = set()
+    for c in sorted(si.WORKLOADS):
+        for s in si.WORKLOADS[c]:
+            key = (s.M, s.N, s.K)
+            if key not in seen:
+                seen.add(key)
+                yield s
+
+
+def sweep(iters: int):
+    dev = torch.device("cuda:0")
+    results = []
+    for s in shapes():
+        g = torch.Generator(device="cpu").manual_seed(s.seed)
+        xq = torch.randint(-127, 128, (s.M, s.K), generator=g, dtype=torch.int8).to(dev)
+        wq = torch.randint(-127, 128, (s.N, s.K), generator=g, dtype=torch.int8).to(dev)
+        sx = torch.rand(s.M, generator=g).to(dev)
+        sw = torch.rand(s.N, generator=g).to(dev)
+        b = torch.zeros(s.N, dtype=torch.bfloat16, device=dev)
+        row = {"M": s.M, "N": s.N, "K": s.K, "ms": {}}
+        for t in range(w8a8.tile_count()):
+            ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t), iters)
+            row["ms"][w8a8.tile_name(t)] = ms
+        best = min(row["ms"], key=row["ms"].get)
+        row["best"] = best
+        row["best_tops"] = 2 * s.M * s.N * s.K / (row["ms"][best] * 1e-3) / 1e12
+        print(json.dumps(row), flush=True)
+        results.append(row)
+    return results
+
+
+def write_table(results, path):
+    names = [w8a8.tile_name(t) for t in range(w8a8.tile_count())]
+    lines = [HEADER, "static const TableEntry kTileTable[] = {"]
+    for r in results:
+        lines.append(f"    {{{r['M']}, {r['M']}, {r['N']}, {r['K']}, {names.index(r['best'])}}},"
+                     f"  // {r['best']} {r['best_tops']:.0f} TOPS")
+    lines.append("    {0, 0, 0, 0, -1},  // sentinel")
+    lines.append("};")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--json")
+    ap.add_argument("--iters", type=int, default=20)
+    a = ap.parse_args()
+    res = sweep(a.iters)
+    write_table(res, a.out)
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump(res, f, indent=1)
+
+
+if __name__ == "__main__":
+    main()

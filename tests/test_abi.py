@@ -1,0 +1,124 @@
+"""The C ABI without a GPU: the library loads, exports every function include/w8a8.h
+declares, and rejects bad arguments before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_14598_amd as w8a8
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "w8a8.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_K, ERR_HIP, ERR_WS, ERR_ARG = range(7)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(w8a8_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(w8a8.library_path()):
+        pytest.fail("libw8a8.so is not built (run python -m paper_2606_14598_amd.build)")
+    return w8a8.load_library()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for must in ("w8a8_quantize_weight", "w8a8_quantize_act", "w8a8_gemm", "w8a8_linear",
+                 "w8a8_gemm_acc_i32"):
+        assert must in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    raw = ctypes.CDLL(w8a8.library_path())
+    for name in declared_functions():
+        assert hasattr(raw, name), f"{name} not exported"
+
+
+def test_no_internal_symbols_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", w8a8.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    funcs = [l.split()[-1] for l in out.splitlines() if " T " in l]
+    assert funcs and all(f.startswith("w8a8_") for f in funcs), funcs
+
+
+def test_status_strings(lib):
+    for st in range(7):
+        assert lib.w8a8_status_string(st)
+    assert lib.w8a8_status_string(99) == b"unknown status"
+
+
+def test_validation_before_launch(lib):
+    P = ctypes.c_void_p
+    fake = P(256)  # never dereferenced: validation fails first
+    # negative sizes
+    assert lib.w8a8_gemm(fake, fake, fake, fake, None, fake, -1, 8, 8, None, 0, None) == ERR_SHAPE
+    assert lib.w8a8_quantize_act(fake, 4, -3, fake, fake, None) == ERR_SHAPE
+    assert lib.w8a8_linear(fake, fake, fake, None, fake, 4, -8, 8, fake, 1 << 20, None) == ERR_SHAPE
+    # K too large for an int32 accumulator
+    assert lib.w8a8_gemm_acc_i32(fake, fake, fake, 4, 4, w8a8.MAX_K + 1, None) == ERR_K
+    assert lib.w8a8_gemm(fake, fake, fake, fake, None, fake, 4, 4, w8a8.MAX_K + 1, None, 0,
+                         None) == ERR_K
+    # NULL pointers
+    assert lib.w8a8_gemm(None, fake, fake, fake, None, fake, 4, 4, 16, None, 0, None) == ERR_NULL
+    assert lib.w8a8_gemm(fake, None, fake, fake, None, fake, 4, 4, 16, None, 0, None) == ERR_NULL
+    assert lib.w8a8_gemm(fake, fake, fake, fake, None, None, 4, 4, 16, None, 0, None) == ERR_NULL
+    assert lib.w8a8_quantize_weight(fake, 4, 16, None, fake, None) == ERR_NULL
+    assert lib.w8a8_quantize_weight(fake, 4, 16, fake, None, None) == ERR_NULL
+    assert lib.w8a8_gemm_acc_i32(fake, fake, None, 4, 4, 16, None) == ERR_NULL
+    # workspace
+    assert lib.w8a8_linear(fake, fake, fake, None, fake, 4, 8, 16, None, 0, None) == ERR_WS
+    need = lib.w8a8_linear_workspace_bytes(4, 8, 16)
+    assert lib.w8a8_linear(fake, fake, fake, None, fake, 4, 8, 16, fake, need - 1, None) == ERR_WS
+    assert lib.w8a8_linear(fake, fake, fake, None, fake, 4, 8, 16, P(256 + 8), need, None) == ERR_WS
+    # unknown tile
+    n = lib.w8a8_tile_count()
+    assert lib.w8a8_gemm_ex(fake, fake, fake, fake, None, fake, 4, 4, 16, None, 0, n,
+                            None) == ERR_ARG
+    assert lib.w8a8_gemm_acc_i32_ex(fake, fake, fake, 4, 4, 16, -2, None) == ERR_ARG
+
+
+def test_empty_is_a_no_op(lib):
+    # M == 0 or N == 0: valid and nothing is launched (works without a GPU)
+    assert lib.w8a8_gemm(None, None, None, None, None, None, 0, 8, 16, None, 0, None) == OK
+    assert lib.w8a8_gemm(None, None, None, None, None, None, 8, 0, 16, None, 0, None) == OK
+    assert lib.w8a8_gemm_acc_i32(None, None, None, 0, 0, 0, None) == OK
+    assert lib.w8a8_linear(None, None, None, None, None, 0, 8, 16, None, 0, None) == OK
+    assert lib.w8a8_quantize_act(None, 0, 16, None, None, None) == OK
+
+
+def test_tile_table_host_logic(lib):
+    n = lib.w8a8_tile_count()
+    assert n >= 4
+    names = [lib.w8a8_tile_name(i).decode() for i in range(n)]
+    assert len(set(names)) == n
+    assert lib.w8a8_tile_name(n) is None
+    for M, N, K in [(1, 4096, 4096), (77, 16384, 4096), (2560, 4096, 4096),
+                    (4608, 12288, 4096), (4625, 4096, 3136), (64, 128, 256)]:
+        t = lib.w8a8_select_tile(M, N, K)
+        assert 0 <= t < n
+    assert lib.w8a8_select_tile(0, 8, 8) == -1
+
+
+def test_workspace_queries(lib):
+    M, N, K = 2560, 4096, 4096
+    need = lib.w8a8_linear_workspace_bytes(M, N, K)
+    assert need >= M * K + 4 * M
+    assert need % 256 == 0 or lib.w8a8_gemm_workspace_bytes(M, N, K) % 256 != 0
+    assert lib.w8a8_linear_workspace_bytes(0, N, K) == 0
+
+
+def test_python_binding_rejects_cpu_tensors():
+    import torch
+    x = torch.zeros(4, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        w8a8.quantize_act(x)
+    with pytest.raises(TypeError):
+        w8a8.quantize_act(x.float())

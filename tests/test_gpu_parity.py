@@ -1,0 +1,298 @@
+"""Parity of the HIP path with the CPU oracle (needs an MI355X).
+
+Every comparison is against the oracle run on the same seeded inputs; nothing the GPU
+produces feeds the oracle. Bars: int8 codes, float32 scales and the int32 accumulator
+bit-exact; bf16 outputs within 1 ulp, all finite, cosine >= 0.99999 (the float32
+epilogue runs in the same order on both sides, so they are in fact expected to match
+bit for bit -- the mismatch count is printed).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth_inputs as si
+import paper_2606_14598_amd as w8a8
+from _helpers import assert_bf16_parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w8a8.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev_bf16(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy()
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+# ---------------------------------------------------------------- quantizer
+
+QUANT_K = [1, 3, 7, 8, 16, 24, 264, 512, 520, 1024, 2048, 3136, 4096, 4104, 8192, 16384,
+           16392, 20000]
+
+
+@pytest.mark.parametrize("K", QUANT_K)
+def test_quantizer_bytes_and_scales_exact(K):
+    """Codes and scale bits equal the oracle's for every kernel variant (register-resident
+    wave/block rows, looped rows, scalar rows)."""
+    say(f"quantizer K={K}")
+    x, _, _ = si.make_inputs((37, K, 1), seed=100 + K, dist="student_t")
+    if K >= 4:
+        x[3] = 0                                                   # zero row
+        x[5] = si.bf16_bits_from_f32(oracle.bf16_to_f32(x[5]) * np.float32(1e-38))
+        x[6] = si.bf16_bits_from_f32(np.where(np.arange(K) % 3 == 0, 1e-36, 7e-39).astype(np.float32))
+        x[7] = si.bf16_bits_from_f32(-np.abs(oracle.bf16_to_f32(x[7])))
+    q_o, s_o = oracle.quantize_rows(x)
+    q, s = w8a8.quantize_act(dev_bf16(x))
+    torch.cuda.synchronize()
+    assert np.array_equal(host(q), q_o)
+    assert np.array_equal(host(s).view(np.uint32), s_o.view(np.uint32))
+    qw, sw = w8a8.quantize_weight(dev_bf16(x))
+    assert np.array_equal(host(qw), q_o) and np.array_equal(host(sw).view(np.uint32),
+                                                             s_o.view(np.uint32))
+
+
+def test_quantizer_unaligned_pointers():
+    K = 256
+    x, _, _ = si.make_inputs((20, K + 1, 1), seed=3)
+    buf = dev_bf16(x.ravel())
+    view = buf[1:1 + 19 * K].view(19, K)     # 2-byte offset: not 16-byte aligned
+    q_o, s_o = oracle.quantize_rows(x.ravel()[1:1 + 19 * K].reshape(19, K))
+    q, s = w8a8.quantize_act(view)
+    assert np.array_equal(host(q), q_o)
+    assert np.array_equal(host(s), s_o)
+
+
+# ---------------------------------------------------------------- int32 accumulator
+
+ACC_SHAPES = [(64, 128, 256), (257, 391, 384), (300, 520, 1040), (1, 1, 16), (33, 65, 4096),
+              (130, 17, 3136), (5, 300, 128), (513, 260, 512)]
+GENERIC_SHAPES = [(45, 77, 269), (3, 5, 1), (70, 140, 264 + 8)]
+
+
+def _acc_case(M, N, K, seed):
+    x, w, _ = si.make_inputs((M, K, N), seed=seed)
+    xq_o, _ = oracle.quantize_rows(x)
+    wq_o, _ = oracle.quantize_rows(w)
+    return xq_o, wq_o, oracle.gemm_acc(xq_o, wq_o)
+
+
+@pytest.mark.parametrize("tile", range(7))
+def test_acc_exact_every_tile(tile):
+    """Every tile configuration gives the exact accumulator on ragged shapes (M, N not
+    multiples of the tile, K tails, single rows/columns)."""
+    if tile >= w8a8.tile_count():
+        pytest.skip("no such tile")
+    for (M, N, K) in ACC_SHAPES + GENERIC_SHAPES:
+        say(f"acc tile={tile} ({w8a8.tile_name(tile)}) M={M} N={N} K={K}")
+        xq_o, wq_o, acc_o = _acc_case(M, N, K, seed=M * 7 + N * 3 + K)
+        acc = w8a8.gemm_acc_i32(torch.from_numpy(xq_o).cuda(), torch.from_numpy(wq_o).cuda(),
+                                tile=tile)
+        assert np.array_equal(host(acc), acc_o), (tile, M, N, K)
+
+
+def test_acc_unaligned_pointers_generic_path():
+    M, N, K = 40, 50, 256
+    xq_o, wq_o, acc_o = _acc_case(M, N, K, seed=77)
+    xb = torch.zeros(M * K + 3, dtype=torch.int8, device="cuda")
+    wb = torch.zeros(N * K + 5, dtype=torch.int8, device="cuda")
+    xb[3:].copy_(torch.from_numpy(xq_o.ravel()))
+    wb[5:].copy_(torch.from_numpy(wq_o.ravel()))
+    acc = w8a8.gemm_acc_i32(xb[3:].view(M, K), wb[5:].view(N, K))
+    assert np.array_equal(host(acc), acc_o)
+
+
+def test_acc_extreme_values_at_max_k():
+    """|acc| reaches 127^2 * K at K = 133144 without wrapping."""
+    K = w8a8.MAX_K
+    xq = torch.full((3, K), 127, dtype=torch.int8, device="cuda")
+    xq[1] = -127
+    wq = torch.full((5, K), 127, dtype=torch.int8, device="cuda")
+    wq[2] = -127
+    acc = host(w8a8.gemm_acc_i32(xq, wq))
+    want = np.outer([127, -127, 127], [127, 127, -127, 127, 127]).astype(np.int64) * K
+    assert np.array_equal(acc.astype(np.int64), want)
+
+
+def test_acc_against_torch_int_mm():
+    """The paper's own reference routine (a library int8 matmul), where ROCm has it."""
+    M, N, K = 256, 384, 512
+    xq_o, wq_o, acc_o = _acc_case(M, N, K, seed=5)
+    xq, wq = torch.from_numpy(xq_o).cuda(), torch.from_numpy(wq_o).cuda()
+    acc = host(w8a8.gemm_acc_i32(xq, wq))
+    assert np.array_equal(acc, acc_o)
+    try:
+        ref = torch._int_mm(xq, wq.t().contiguous())
+    except Exception as e:  # noqa: BLE001
+        pytest.skip(f"torch._int_mm unavailable: {e}")
+    assert np.array_equal(acc, host(ref))
+
+
+# ---------------------------------------------------------------- bf16 output
+
+LINEAR_SMALL = [(64, 256, 128, "outlier"), (257, 384, 391, "student_t"),
+                (130, 3136, 260, "gelu"), (1, 4096, 130, "outlier"), (77, 264, 64, "outlier"),
+                (45, 269, 77, "student_t")]
+
+
+@pytest.mark.parametrize("M,K,N,dist", LINEAR_SMALL)
+def test_linear_full_compare_small(M, K, N, dist):
+    say(f"linear small M={M} K={K} N={N} {dist}")
+    x, w, b = si.make_inputs((M, K, N), seed=M + K + N, dist=dist)
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, xq_o, sx_o, acc_o = oracle.linear(x, wq_o, sw_o, b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    assert np.array_equal(host(wq), wq_o) and np.array_equal(host(sw), sw_o)
+    y = w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b))
+    st = assert_bf16_parity(host_bits(y), y_o, f"linear {M}x{K}x{N}")
+    say("  ", st)
+    # gemm on the oracle-checked quantized activations, every tile
+    xq, sx = w8a8.quantize_act(dev_bf16(x))
+    for t in range(w8a8.tile_count()):
+        y2 = w8a8.gemm(xq, sx, wq, sw, dev_bf16(b), tile=t)
+        assert np.array_equal(host_bits(y2), host_bits(y)), t
+    # without bias
+    y_nb = w8a8.gemm(xq, sx, wq, sw, None)
+    assert_bf16_parity(host_bits(y_nb), oracle.epilogue(acc_o, sx_o, sw_o, None), "no bias")
+
+
+def test_linear_k_zero_gives_bias():
+    M, N = 9, 33
+    _, _, b = si.make_inputs((1, 8, N), seed=1)
+    x = torch.empty((M, 0), dtype=torch.bfloat16, device="cuda")
+    wq = torch.empty((N, 0), dtype=torch.int8, device="cuda")
+    sw = torch.zeros(N, dtype=torch.float32, device="cuda")
+    y = w8a8.linear(x, wq, sw, dev_bf16(b))
+    assert np.array_equal(host_bits(y), np.broadcast_to(b, (M, N)))
+
+
+def test_empty_shapes():
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    wq = torch.zeros((8, 64), dtype=torch.int8, device="cuda")
+    sw = torch.ones(8, dtype=torch.float32, device="cuda")
+    assert w8a8.linear(x, wq, sw).shape == (0, 8)
+    q, s = w8a8.quantize_act(x)
+    assert q.shape == (0, 64) and s.shape == (0,)
+
+
+def test_zero_and_tiny_tokens_give_bias():
+    """Token 0 is zero and token 1 has a ~ 5e-39 (127/a overflows): both are zero rows and
+    give the bias exactly. Token 2 has a ~ 5e-37: a subnormal scale, kept on both sides."""
+    M, K, N = 40, 512, 96
+    x, w, b = si.make_inputs((M, K, N), seed=21)
+    x[0] = 0
+    x[1] = si.bf16_bits_from_f32(oracle.bf16_to_f32(x[1]) * np.float32(1e-40))
+    x[2] = si.bf16_bits_from_f32(oracle.bf16_to_f32(x[2]) * np.float32(1e-38))
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, _, sx_o, _ = oracle.linear(x, wq_o, sw_o, b)
+    assert sx_o[0] == 0 and sx_o[1] == 0
+    assert 0 < sx_o[2] < np.finfo(np.float32).tiny
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    y = host_bits(w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b)))
+    assert np.array_equal(y[0], b) and np.array_equal(y[1], b)
+    assert_bf16_parity(y, y_o, "zero/tiny tokens")
+
+
+def test_guard_bands_untouched():
+    """Canary elements around the output and the quantized activations stay intact."""
+    M, K, N = 131, 1040, 262
+    x, w, b = si.make_inputs((M, K, N), seed=31)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    pad = 4096
+    ybuf = torch.full((M * N + 2 * pad,), 1.5, dtype=torch.bfloat16, device="cuda")
+    y = ybuf[pad:pad + M * N].view(M, N)
+    w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b), out=y)
+    qbuf = torch.full((M * K + 2 * pad,), 99, dtype=torch.int8, device="cuda")
+    sbuf = torch.full((M + 2 * pad,), -3.0, dtype=torch.float32, device="cuda")
+    lib = w8a8.load_library()
+    import ctypes
+    st = lib.w8a8_quantize_act(ctypes.c_void_p(dev_bf16(x).data_ptr()), M, K,
+                               ctypes.c_void_p(qbuf[pad:].data_ptr()),
+                               ctypes.c_void_p(sbuf[pad:].data_ptr()),
+                               ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert st == 0
+    yb = ybuf.float().cpu().numpy()
+    assert np.all(yb[:pad] == 1.5) and np.all(yb[pad + M * N:] == 1.5)
+    qb = host(qbuf)
+    assert np.all(qb[:pad] == 99) and np.all(qb[pad + M * K:] == 99)
+    sb = host(sbuf)
+    assert np.all(sb[:pad] == -3.0) and np.all(sb[pad + M:] == -3.0)
+
+
+def test_deterministic_and_stream_independent():
+    shp = si.workload(1, "attn_proj")
+    x, w, b = si.make_inputs(shp)
+    xd, bd = dev_bf16(x), dev_bf16(b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    y0 = host_bits(w8a8.linear(xd, wq, sw, bd))
+    for _ in range(5):
+        assert np.array_equal(host_bits(w8a8.linear(xd, wq, sw, bd)), y0)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y1 = w8a8.linear(xd, wq, sw, bd)
+    s.synchronize()
+    assert np.array_equal(host_bits(y1), y0)
+
+
+# ---------------------------------------------------------------- full sizes, sampled
+
+FULL_SHAPES = [(c, s.name) for c in (1, 2, 3, 4) for s in si.WORKLOADS[c]]
+
+
+def _sample(n, rng, tile=256):
+    base = {0, 1, 31, 32, 127, 128, tile - 1, tile, n - 2, n - 1}
+    base |= set(rng.integers(0, n, size=6).tolist())
+    return np.array(sorted(i for i in base if 0 <= i < n))
+
+
+@pytest.mark.parametrize("config,name", FULL_SHAPES)
+def test_full_size_sampled(config, name):
+    """At the benchmark's shapes, through the same entry point and tile the benchmark
+    times: weight codes/scales exact in full; bf16 outputs and int32 accumulators of
+    sampled whole rows and whole columns against the oracle (which computes exactly
+    those rows/columns: per-token quantization makes rows independent)."""
+    shp = si.workload(config, name)
+    say(f"full-size {config}/{name}: M={shp.M} K={shp.K} N={shp.N} tile="
+        f"{w8a8.tile_name(w8a8.select_tile(shp.M, shp.N, shp.K))}")
+    x, w, b = si.make_inputs(shp)
+    wq_o, sw_o = oracle.quantize_rows(w)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    assert np.array_equal(host(wq), wq_o) and np.array_equal(host(sw), sw_o)
+    xd = dev_bf16(x)
+    y = host_bits(w8a8.linear(xd, wq, sw, dev_bf16(b)))
+    xq, sx = w8a8.quantize_act(xd)
+    acc = w8a8.gemm_acc_i32(xq, wq)
+    xq_h = host(xq)
+    rng = np.random.default_rng(shp.seed)
+    rows = _sample(shp.M, rng)
+    cols = _sample(shp.N, rng)
+    # rows: all N outputs of sampled tokens
+    y_r, xq_r, sx_r, acc_r = oracle.linear(x[rows], wq_o, sw_o, b)
+    assert np.array_equal(xq_h[rows], xq_r)
+    assert np.array_equal(host(sx)[rows], sx_r)
+    assert np.array_equal(host(acc)[rows], acc_r)
+    st = assert_bf16_parity(y[rows], y_r, f"{name} rows")
+    # columns: all M outputs of sampled channels
+    y_c, _, _, acc_c = oracle.linear(x, wq_o[cols], sw_o[cols], b[cols])
+    assert np.array_equal(host(acc)[:, cols], acc_c)
+    st2 = assert_bf16_parity(y[:, cols], y_c, f"{name} cols")
+    say("   rows", st, "cols", st2)
