@@ -53,16 +53,21 @@ def shapes():
                 yield s
 
 
+def _dev_bf16(bits, dev):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
 def sweep(iters: int):
+    """Time every tile on every workload shape, on the workload's own synthetic inputs
+    quantized by the library: the matrix cores' sustained rate depends on the operand
+    bits (switching power), so uniform random or constant codes would mislead."""
     dev = torch.device("cuda:0")
     results = []
     for s in shapes():
-        g = torch.Generator(device="cpu").manual_seed(s.seed)
-        xq = torch.randint(-127, 128, (s.M, s.K), generator=g, dtype=torch.int8).to(dev)
-        wq = torch.randint(-127, 128, (s.N, s.K), generator=g, dtype=torch.int8).to(dev)
-        sx = torch.rand(s.M, generator=g).to(dev)
-        sw = torch.rand(s.N, generator=g).to(dev)
-        b = torch.zeros(s.N, dtype=torch.bfloat16, device=dev)
+        x, w, bb = si.make_inputs(s)
+        xq, sx = w8a8.quantize_act(_dev_bf16(x, dev))
+        wq, sw = w8a8.quantize_weight(_dev_bf16(w, dev))
+        b = _dev_bf16(bb, dev)
         row = {"M": s.M, "N": s.N, "K": s.K, "ms": {}}
         for t in range(w8a8.tile_count()):
             ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t), iters)
