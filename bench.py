@@ -183,9 +183,10 @@ def comparators(shp, xd, wd, bd, wq, sw, iters):
 
 
 def cpu_baseline(shp, x, w, b, budget_s: float = 12.0) -> dict:
-    """The CPU oracle (as it stands) on a bounded row sample of the workload's linear:
+    """The CPU oracle (as it stands) on a bounded sample of the workload's linear:
     per-token quantization, exact integer product and epilogue for `rows` tokens against
-    the full weight. Reported in the metric's unit (int8 TOP/s)."""
+    the full weight, repeated until about budget_s seconds have passed. Reported in the
+    metric's unit (int8 TOP/s)."""
     import numpy as np
     import oracle
     wq_o, sw_o = oracle.quantize_rows(w)
@@ -196,14 +197,18 @@ def cpu_baseline(shp, x, w, b, budget_s: float = 12.0) -> dict:
     t = time.perf_counter() - t0
     rows = int(min(shp.M, max(rows, rows * budget_s / max(t, 1e-3))))
     rows = max(threads, rows // threads * threads)
-    t0 = time.perf_counter()
-    oracle.linear(np.ascontiguousarray(x[:rows]), wq_o, sw_o, b)
-    t = time.perf_counter() - t0
-    ops = gemm_ops(rows, shp.N, shp.K)
-    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": threads,
+    xs = np.ascontiguousarray(x[:rows])
+    reps, total = 0, 0.0
+    while total < budget_s and reps < 1000:
+        t0 = time.perf_counter()
+        oracle.linear(xs, wq_o, sw_o, b)
+        total += time.perf_counter() - t0
+        reps += 1
+    ops = gemm_ops(rows, shp.N, shp.K) * reps
+    return {"value": round(ops / total / 1e12, 6), "unit": "TOPS", "cores": threads,
             "kind": "oracle",
-            "sample": f"{rows} of {shp.M} tokens of the {shp.M}x{shp.K}x{shp.N} linear "
-                      f"(quantize + int8 product + epilogue), {t:.1f} s"}
+            "sample": f"{reps} x {rows} of {shp.M} tokens of the {shp.M}x{shp.K}x{shp.N} "
+                      f"linear (quantize + int8 product + epilogue), {total:.1f} s"}
 
 
 # ------------------------------------------------------------------ main measurement
@@ -233,6 +238,15 @@ def run(args) -> dict:
                                                   (xd, xq, sx, wq, sw, bd, y, ws))
     nws = ws.numel()
 
+    lws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+    a_lws, n_lws = P(lws.data_ptr()), lws.numel()
+
+    def step():
+        # The product entry point: per-token quantizer + fused GEMM, back to back.
+        st = lib.w8a8_linear(a_x, a_wq, a_sw, a_b, a_y, M, N, K, a_lws, n_lws, sp)
+        if st:
+            raise RuntimeError(f"w8a8_linear status {st}")
+
     def quant():
         st = lib.w8a8_quantize_act(a_x, M, K, a_xq, a_sx, sp)
         if st:
@@ -243,26 +257,25 @@ def run(args) -> dict:
         if st:
             raise RuntimeError(f"w8a8_gemm status {st}")
 
-    for _ in range(args.warmup):
-        quant()
-        gemm()
-    torch.cuda.synchronize()
+    def timed(fn, n):
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(n):
+            fn()
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / n
 
+    for _ in range(args.warmup):
+        step()
     K_steps = args.steps
-    g0 = [torch.cuda.Event(enable_timing=True) for _ in range(K_steps)]
-    g1 = [torch.cuda.Event(enable_timing=True) for _ in range(K_steps)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(K_steps):
-        quant()
-        g0[i].record(stream)
-        gemm()
-        g1[i].record(stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / K_steps
-    gemm_ms = sum(a.elapsed_time(bb) for a, bb in zip(g0, g1)) / K_steps
+    ms_step = timed(step, K_steps)
+    # The dominant kernel's mean launch duration: the same GEMM launch back to back on
+    # the same stream, HIP events around the loop.
+    quant()
+    gemm_ms = timed(gemm, K_steps)
+    quant_ms = timed(quant, K_steps)
 
     ops = gemm_ops(M, N, K)
     value_tops = ops / (ms_step * 1e-3) / 1e12
@@ -284,7 +297,8 @@ def run(args) -> dict:
         "data": "synthetic",
         "config": {"workload": f"DiT attention-projection W8A8 linear, 768px-like sequence: "
                                f"M={M} tokens, K={K}, N={N}, bf16 in/out with bias",
-                   "M": M, "K": K, "N": N, "timed": "quantize_act + fused int8 GEMM/epilogue",
+                   "M": M, "K": K, "N": N,
+                   "timed": "w8a8_linear: per-token quantizer + fused int8 GEMM/epilogue",
                    "tile": w8a8.tile_name(tile), "seed": shp.seed},
         "pct_of_int8_peak": round(100 * value_tops / PEAK_INT8_TOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2),
@@ -293,15 +307,18 @@ def run(args) -> dict:
                      "traffic": traffic,
                      "kernel": f"gemm_i8 {w8a8.tile_name(tile)} (int8 ops counted 2 per MAC)",
                      "gemm_ms": round(gemm_ms, 5),
+                     "duration_from": "HIP events around back-to-back launches of this GEMM "
+                                      "on the benchmark stream",
                      "algorithmic_bytes": gemm_bytes(M, N, K),
                      "source": gemm_source_hash()},
     }
 
     if not args.no_extra:
         rec["health_gate"] = health
-        quant_ms = ms_step - gemm_ms
-        rec["quantizer"] = {"ms_approx": round(quant_ms, 5),
-                            "GB_s_approx": round(quant_bytes(M, K) / (quant_ms * 1e-3) / 1e9, 1)}
+        rec["quantizer"] = {"ms": round(quant_ms, 5),
+                            "GB_s": round(quant_bytes(M, K) / (quant_ms * 1e-3) / 1e9, 1),
+                            "frac_of_hbm": round(quant_bytes(M, K) / (quant_ms * 1e-3) / 1e9
+                                                 / PEAK_HBM_GBS, 4)}
         it = max(10, args.steps)
         comp = comparators(shp, xd, wd, bd, wq, sw, it)
         comp["speedup_vs_bf16"] = round(comp["bf16_linear_ms"] / ms_step, 3)

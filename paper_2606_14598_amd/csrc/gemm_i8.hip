@@ -93,7 +93,8 @@ struct KParams {
     GemmArgs a;
     int tiles_m, tiles_n;
     int gm;          // token-tiles per raster group
-    int out_vec;     // output rows 16-byte aligned with N % 4 == 0, scale/bias aligned
+    int out_vec;     // 0: scalar stores; 1: rows 8-byte (bf16) / 16-byte (int32) aligned
+                     // with N % 4 == 0; 2 (bf16): rows 16-byte aligned with N % 8 == 0
 };
 
 // Epilogue of one wavefront's (FN*32 channels) x (FM*32 tokens) accumulator tile whose
@@ -165,6 +166,66 @@ __device__ __forceinline__ void store_tile(const i32x16 (&acc)[FN][FM], const KP
                     }
                 }
             }
+        }
+    }
+}
+
+// bf16 epilogue through LDS, for outputs whose rows are 16-byte aligned with N % 8 == 0
+// (kp.out_vec == 2). The wavefront converts one 32-token chunk of its tile at a time into
+// a private LDS region of 32 rows x (2*WTN + 16) bytes (the pad spreads the 32 rows over
+// the banks), then writes the chunk back to global memory row by row with 16-byte
+// stores, so every store instruction covers whole contiguous row segments. The token
+// scales, channel scales and bias (as fp32) of the tile come from LDS (t_sx, t_sw, t_b,
+// indexed from the wavefront's first token / channel; out-of-range entries are 0).
+// Needs a barrier before it (the region overlaps the panel stages) and
+// 32 * (2*WTN + 16) bytes of LDS per wavefront.
+template <int FN, int FM>
+__device__ __forceinline__ void store_tile_bf16_lds(const i32x16 (&acc)[FN][FM],
+                                                    const KParams &kp, int64_t m_base,
+                                                    int64_t n_base, int lane,
+                                                    int8_t *region, const float *t_sx,
+                                                    const float *t_sw, const float *t_b) {
+    constexpr int WTN = FN * 32;
+    constexpr int RS = 2 * WTN + 16;          // region row stride in bytes
+    constexpr int CPRO = WTN / 8;             // 16-byte chunks per output row
+    const GemmArgs &a = kp.a;
+    const int64_t M = a.M, N = a.N;
+    const int h = lane >> 5, r = lane & 31;
+    uint16_t *out = static_cast<uint16_t *>(a.out);
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+        const float sxm = t_sx[j * 32 + r];
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                // This lane's channels: c .. c+3 of the wavefront's tile.
+                const int c = i * 32 + g * 8 + h * 4;
+                const f32x4 sw4 = *reinterpret_cast<const f32x4 *>(t_sw + c);
+                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(t_b + c);
+                uint16_t hv[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float sc = sxm * sw4[e];
+                    const float y = __builtin_fmaf((float)acc[i][j][4 * g + e], sc, b4[e]);
+                    hv[e] = __builtin_bit_cast(uint16_t, (__bf16)y);
+                }
+                uint2 pk;
+                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                *reinterpret_cast<uint2 *>(region + r * RS + c * 2) = pk;
+            }
+        }
+        // Read back whole rows: lane-chunk q covers row q / CPRO, 8 channels at q % CPRO.
+#pragma unroll
+        for (int q0 = 0; q0 < 32 * CPRO; q0 += 64) {
+            const int q = q0 + lane;
+            const int row = q / CPRO, ch = q % CPRO;
+            const uint4 v = *reinterpret_cast<const uint4 *>(region + row * RS + ch * 16);
+            const int64_t mm = m_base + j * 32 + row;
+            const int64_t nn = n_base + ch * 8;
+            if (mm < M && nn < N)
+                *reinterpret_cast<uint4 *>(out + mm * N + nn) = v;
         }
     }
 }
@@ -312,19 +373,28 @@ __device__ __forceinline__ void barrier_nofence() {
 template <int TM, int TN, int BK, int WM, int WN, int S, int EPI>
 __global__ void __launch_bounds__(WM *WN * 64)
 gemm_i8_lds_kernel(KParams kp) {
-    constexpr int NT = WM * WN * 64;
+    constexpr int NW = WM * WN;                // wavefronts
     constexpr int WTM = TM / WM, WTN = TN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
     constexpr int CPR = BK / 16;
-    constexpr int RPL = NT / CPR;              // rows covered by one load instruction
-    constexpr int LW = TN / RPL, LX = TM / RPL;
-    constexpr int NV = LW + LX;                // loads per thread per panel
+    constexpr int RPI = 64 / CPR;              // rows filled by one load instruction
+    constexpr int IW = TN / RPI, IX = TM / RPI;   // load instructions per panel (whole WG)
+    constexpr int NI = IW + IX;
+    constexpr int NV = (NI + NW - 1) / NW;     // load instructions per wavefront per panel
     constexpr int STAGE = (TN + TM) * BK;
     constexpr int KS = BK / 32;
     static_assert(FM >= 1 && FN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-    static_assert(RPL % 32 == 0 && TN % RPL == 0 && TM % RPL == 0, "load split");
+    static_assert(TN % RPI == 0 && TM % RPI == 0, "load split");
     static_assert(S >= 2 && (S - 2) * NV <= 63, "stages");
-    __shared__ __attribute__((aligned(1024))) int8_t smem[S * STAGE];
+    // One LDS object holds the panel stages and, behind them, the epilogue vectors of the
+    // tile (token scales, channel scales, bias as fp32). A single object keeps the
+    // compiler's LDS-DMA tracking exact: with a second LDS variable it makes every
+    // ds_read wait for all in-flight panel loads.
+    constexpr int NSC = EPI == EPI_BF16 ? 1 : 0;
+    __shared__ __attribute__((aligned(1024))) int8_t smem[S * STAGE + NSC * (TM + 2 * TN) * 4];
+    float *const t_sx = reinterpret_cast<float *>(smem + S * STAGE);
+    float *const t_sw = t_sx + NSC * TM;
+    float *const t_b = t_sw + NSC * TN;
 
     const GemmArgs &a = kp.a;
     const int lane = threadIdx.x & 63;
@@ -342,11 +412,11 @@ gemm_i8_lds_kernel(KParams kp) {
     const __amdgpu_buffer_rsrc_t rx_rsrc = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(a.xq + m0 * K), (short)0, rows_x * K, kRsrcWord3);
 
-    // This lane's source in every load: row r0 + i*RPL, logical chunk kc0.
-    const int c0 = wave * 64 + lane;
-    const int r0 = c0 / CPR;
-    const int kc0 = (c0 % CPR) ^ swz<BK>(r0);
-    const int voff0 = r0 * K + kc0 * 16;
+    // Load instruction g (0 <= g < NI; the first IW fill the weight part of a stage, the
+    // rest the activation part) is issued by wavefront g % NW; its lane l fills LDS chunk
+    // 64*g' + l of that part (g' = g or g - IW), i.e. row RPI*g' + l/CPR, physical chunk
+    // l % CPR, and so fetches logical chunk (l % CPR) ^ swz(row) of that row.
+    const int lrow = lane / CPR, lchunk = lane % CPR;
 
     // This lane's fragment offset inside a stage for K-step ks (the same for every
     // 32-row fragment, whose base differs by a constant).
@@ -367,31 +437,46 @@ gemm_i8_lds_kernel(KParams kp) {
 
     const int nk = (K + BK - 1) / BK;
 
-    // Per-lane source offset of panel kt's first load and the stride between loads.
-    // Only the last panel can reach past K; there, lanes whose chunk starts at or past K
-    // read from an offset beyond the buffer and get zeros. Panels kt >= nk read zeros
-    // everywhere: the loop requests them to stay branch-free, into stages nobody reads.
-    auto panel_src = [&](int kt, int &base, int &step) {
-        const int k0 = kt * BK;
-        const bool live = (kt < nk) & ((k0 + BK <= K) | (k0 + kc0 * 16 < K));
-        base = live ? voff0 + k0 : kOOB;
-        step = live ? RPL * K : 0;
-    };
-    // Loads [I0, I1) of the NV loads of one panel into the stage at byte offset so.
-    auto issue = [&](auto i0c, auto i1c, int base, int step, int so) {
+    // Loads [I0, I1) of this wavefront's NV load instructions of panel kt into the stage
+    // at byte offset so. Only the last panel can reach past K; there, lanes whose chunk
+    // starts at or past K read from an offset beyond the buffer and get zeros. Panels
+    // kt >= nk read zeros everywhere: the loop requests them to stay branch-free, into
+    // stages nobody reads.
+    auto issue = [&](auto i0c, auto i1c, int kt, int so) {
         constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
-        int8_t *dst = smem + so + wave * 64 * 16;
+        const int k0 = kt * BK;
+        const bool full = (kt < nk) & (k0 + BK <= K);
+        const bool inrange = kt < nk;
 #pragma unroll
         for (int i = I0; i < I1; ++i) {
-            if (i < LW)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rw_rsrc, (__attribute__((address_space(3))) void *)(dst + i * NT * 16), 16,
-                    base + i * step, 0, 0, 0);
+            const int g = i * NW + wave;
+            if (i * NW + NW > NI && g >= NI)
+                break;                                       // wave-uniform
+            const bool isw = g < IW;
+            const int gg = isw ? g : g - IW;
+            const int row = gg * RPI + lrow;
+            const int kc = lchunk ^ swz<BK>(row);
+            const bool ok = full | (inrange & (k0 + kc * 16 < K));
+            const int off = ok ? row * K + k0 + kc * 16 : kOOB;
+            int8_t *dst = smem + so + (isw ? 0 : TN * BK) + gg * 1024;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                isw ? rw_rsrc : rx_rsrc, (__attribute__((address_space(3))) void *)dst, 16,
+                off, 0, 0, 0);
+        }
+    };
+
+    // Wait until at most `younger` panels' loads of this wavefront are in flight. When NI
+    // is not a multiple of NW the last NW - NI % NW wavefronts issue one load fewer per
+    // panel, so their count differs (a wave-uniform branch).
+    auto wait_loads = [&](auto youngerc) {
+        constexpr int Y = decltype(youngerc)::value;
+        if constexpr (NI % NW == 0) {
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(Y * NV));
+        } else {
+            if (wave < NI % NW)
+                __builtin_amdgcn_s_waitcnt(waitcnt_vm(Y * NV));
             else
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rx_rsrc,
-                    (__attribute__((address_space(3))) void *)(dst + TN * BK + (i - LW) * NT * 16),
-                    16, base + (i - LW) * step, 0, 0, 0);
+                __builtin_amdgcn_s_waitcnt(waitcnt_vm(Y * (NV - 1)));
         }
     };
 
@@ -414,7 +499,7 @@ gemm_i8_lds_kernel(KParams kp) {
     constexpr int NM = FN * FM, NR = FN + FM;
     constexpr int VPS = (NV + KS - 1) / KS;   // loads per K-step
     constexpr int G = NM >= 4 ? 4 : NM;       // groups per K-step
-    auto kstep = [&](auto ksc, int so, int base, int step, int so_load) {
+    auto kstep = [&](auto ksc, int so, int kt_load, int so_load) {
         constexpr int ks = decltype(ksc)::value;
         [&]<int... g>(std::integer_sequence<int, g...>) {
             ([&] {
@@ -433,8 +518,8 @@ gemm_i8_lds_kernel(KParams kp) {
                 }
                 constexpr int va = ks * VPS + g * VPS / G, vb = ks * VPS + (g + 1) * VPS / G;
                 constexpr int v0 = va < NV ? va : NV, v1 = vb < NV ? vb : NV;
-                issue(std::integral_constant<int, v0>{}, std::integral_constant<int, v1>{}, base,
-                      step, so_load);
+                issue(std::integral_constant<int, v0>{}, std::integral_constant<int, v1>{}, kt_load,
+                      so_load);
                 __builtin_amdgcn_sched_barrier(0);
                 constexpr int q0 = g * NM / G, q1 = (g + 1) * NM / G;
 #pragma unroll
@@ -446,34 +531,82 @@ gemm_i8_lds_kernel(KParams kp) {
         }(std::make_integer_sequence<int, G>{});
     };
 
+    // Tile vectors for the epilogue: fetched now, parked in LDS after the prologue (their
+    // latency hides behind the first panel's).
+    constexpr int NT = NW * 64;
+    constexpr int VSX = (TM + NT - 1) / NT, VSW = (TN + NT - 1) / NT;
+    float r_sx[VSX], r_sw[VSW], r_b[VSW];
+    if constexpr (EPI == EPI_BF16) {
+#pragma unroll
+        for (int v = 0; v < VSX; ++v) {
+            const int idx = v * NT + (int)threadIdx.x;
+            r_sx[v] = (idx < TM && m0 + idx < M) ? a.sx[m0 + idx] : 0.0f;
+        }
+#pragma unroll
+        for (int v = 0; v < VSW; ++v) {
+            const int idx = v * NT + (int)threadIdx.x;
+            const bool in = idx < TN && n0 + idx < N;
+            r_sw[v] = in ? a.sw[n0 + idx] : 0.0f;
+            r_b[v] = (in && a.bias) ? __uint_as_float((uint32_t)a.bias[n0 + idx] << 16) : 0.0f;
+        }
+    }
+    auto park_vectors = [&]() {
+        if constexpr (EPI == EPI_BF16) {
+#pragma unroll
+            for (int v = 0; v < VSX; ++v) {
+                const int idx = v * NT + (int)threadIdx.x;
+                if (idx < TM)
+                    t_sx[idx] = r_sx[v];
+            }
+#pragma unroll
+            for (int v = 0; v < VSW; ++v) {
+                const int idx = v * NT + (int)threadIdx.x;
+                if (idx < TN) {
+                    t_sw[idx] = r_sw[v];
+                    t_b[idx] = r_b[v];
+                }
+            }
+            // The next (fence-free) barrier publishes these stores: complete them first.
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        }
+    };
+
     if (nk > 0) {
         // Prologue: panels 0 .. S-2 into stages 0 .. S-2; wait for panel 0.
 #pragma unroll
-        for (int p = 0; p < S - 1; ++p) {
-            int base, step;
-            panel_src(p, base, step);
-            issue(std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{}, base, step,
+        for (int p = 0; p < S - 1; ++p)
+            issue(std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{}, p,
                   p * STAGE);
-        }
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * NV));
+        wait_loads(std::integral_constant<int, S - 2>{});
+        park_vectors();
         barrier_nofence();
         int st = 0;            // stage of panel kt
         int ld = S - 1;        // stage of panel kt + S - 1
         for (int kt = 0; kt < nk; ++kt) {
-            int base, step;
-            panel_src(kt + S - 1, base, step);
             read_frags(st * STAGE, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
             [&]<int... ks>(std::integer_sequence<int, ks...>) {
-                (kstep(std::integral_constant<int, ks>{}, st * STAGE, base, step, ld * STAGE), ...);
+                (kstep(std::integral_constant<int, ks>{}, st * STAGE, kt + S - 1, ld * STAGE), ...);
             }(std::make_integer_sequence<int, KS>{});
             // Panel kt+1 has landed once at most the S-2 younger panels are in flight.
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * NV));
+            wait_loads(std::integral_constant<int, S - 2>{});
             barrier_nofence();
             st = (st + 1 == S) ? 0 : st + 1;
             ld = (ld + 1 == S) ? 0 : ld + 1;
         }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // the zero-filling tail loads
+    } else {
+        park_vectors();
+    }
+    if constexpr (EPI == EPI_BF16) {
+        static_assert(NW * 32 * (2 * WTN + 16) <= S * STAGE, "epilogue staging");
+        if (kp.out_vec == 2) {
+            barrier_nofence();   // every wavefront is done reading the panel stages
+            store_tile_bf16_lds<FN, FM>(acc, kp, m0 + wm * WTM, n0 + wn * WTN, lane,
+                                        smem + wave * 32 * (2 * WTN + 16), t_sx + wm * WTM,
+                                        t_sw + wn * WTN, t_b + wn * WTN);
+            return;
+        }
     }
     store_tile<FN, FM, EPI>(acc, kp, m0 + wm * WTM, n0 + wn * WTN, lane);
 }
@@ -488,28 +621,34 @@ struct Tile {
     static constexpr int threads = WM * WN * 64;
     static constexpr int lds = (PIPE ? S : 2) * (TM + TN) * BK;
 
-    static hipError_t launch(Epilogue epi, bool vec, const KParams &kp, hipStream_t s) {
+    // Aligned operands only (16-byte pointers, K % 16 == 0); launch_gemm sends the rest
+    // to the generic tile.
+    static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
         const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n)), block(threads);
         if constexpr (PIPE) {
-            if (vec) {
-                if (epi == EPI_BF16)
-                    hipLaunchKernelGGL((gemm_i8_lds_kernel<TM, TN, BK, WM, WN, S, EPI_BF16>), grid, block, 0, s, kp);
-                else
-                    hipLaunchKernelGGL((gemm_i8_lds_kernel<TM, TN, BK, WM, WN, S, EPI_I32>), grid, block, 0, s, kp);
-                return hipGetLastError();
-            }
-        }
-        if (vec) {
+            if (epi == EPI_BF16)
+                hipLaunchKernelGGL((gemm_i8_lds_kernel<TM, TN, BK, WM, WN, S, EPI_BF16>), grid, block, 0, s, kp);
+            else
+                hipLaunchKernelGGL((gemm_i8_lds_kernel<TM, TN, BK, WM, WN, S, EPI_I32>), grid, block, 0, s, kp);
+        } else {
             if (epi == EPI_BF16)
                 hipLaunchKernelGGL((gemm_i8_kernel<TM, TN, BK, WM, WN, true, EPI_BF16>), grid, block, 0, s, kp);
             else
                 hipLaunchKernelGGL((gemm_i8_kernel<TM, TN, BK, WM, WN, true, EPI_I32>), grid, block, 0, s, kp);
-        } else {
-            if (epi == EPI_BF16)
-                hipLaunchKernelGGL((gemm_i8_kernel<TM, TN, BK, WM, WN, false, EPI_BF16>), grid, block, 0, s, kp);
-            else
-                hipLaunchKernelGGL((gemm_i8_kernel<TM, TN, BK, WM, WN, false, EPI_I32>), grid, block, 0, s, kp);
         }
+        return hipGetLastError();
+    }
+};
+
+// Unaligned operands or K % 16 != 0: the register-staged kernel with byte loads.
+struct GenericTile {
+    static constexpr int tm = 128, tn = 128;
+    static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
+        const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n)), block(256);
+        if (epi == EPI_BF16)
+            hipLaunchKernelGGL((gemm_i8_kernel<128, 128, 128, 2, 2, false, EPI_BF16>), grid, block, 0, s, kp);
+        else
+            hipLaunchKernelGGL((gemm_i8_kernel<128, 128, 128, 2, 2, false, EPI_I32>), grid, block, 0, s, kp);
         return hipGetLastError();
     }
 };
@@ -517,7 +656,7 @@ struct Tile {
 struct TileEntry {
     TileInfo info;
     int gm;
-    hipError_t (*launch)(Epilogue, bool, const KParams &, hipStream_t);
+    hipError_t (*launch)(Epilogue, const KParams &, hipStream_t);
 };
 
 #define W8A8_TILE(NAME, TM, TN, BK, WM, WN, GM, S)                                          \
@@ -538,6 +677,10 @@ const TileEntry kTiles[] = {
     W8A8_TILE("m128n128k64w2x2s4", 128, 128, 64, 2, 2, 8, 4),
     W8A8_TILE("m256n256k64w2x4s4", 256, 256, 64, 2, 4, 8, 4),
     W8A8_TILE("m128n128k128w2x2s3", 128, 128, 128, 2, 2, 8, 3),
+    W8A8_TILE("m160n256k128w1x4s3", 160, 256, 128, 1, 4, 8, 3),
+    W8A8_TILE("m160n256k64w1x4s4", 160, 256, 64, 1, 4, 8, 4),
+    W8A8_TILE("m288n256k128w3x4s2", 288, 256, 128, 3, 4, 8, 2),
+    W8A8_TILE("m288n256k64w3x4s3", 288, 256, 64, 3, 4, 8, 3),
     W8A8_TILE("m128n128k128w2x2", 128, 128, 128, 2, 2, 8, 0),
     W8A8_TILE("m64n128k128w1x4", 64, 128, 128, 1, 4, 8, 0),
     W8A8_TILE("m32n128k128w1x4", 32, 128, 128, 1, 4, 8, 0),
@@ -557,17 +700,17 @@ int fallback_tile(int64_t M, int64_t N, int64_t K) {
     (void)K;
     // Prefer the largest tile that still gives at least one workgroup per CU.
     const int64_t cus = 256;
-    for (int id : {0, 2, 3, 4, 8}) {
+    for (int id : {0, 2, 3, 4, 12}) {
         const TileInfo &t = kTiles[id].info;
         const int64_t tiles = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
         if (tiles >= cus)
             return id;
     }
     if (M <= 32)
-        return 10;
+        return 14;
     if (M <= 64)
-        return 9;
-    return 8;
+        return 13;
+    return 12;
 }
 
 }  // namespace
@@ -596,21 +739,23 @@ hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *
                        size_t ws_bytes, hipStream_t stream) {
     (void)ws; (void)ws_bytes;
     const TileEntry &t = kTiles[id];
+    const int tm = vec ? t.info.tm : GenericTile::tm;
+    const int tn = vec ? t.info.tn : GenericTile::tn;
     KParams kp;
     kp.a = a;
-    kp.tiles_m = (int)((a.M + t.info.tm - 1) / t.info.tm);
-    kp.tiles_n = (int)((a.N + t.info.tn - 1) / t.info.tn);
+    kp.tiles_m = (int)((a.M + tm - 1) / tm);
+    kp.tiles_n = (int)((a.N + tn - 1) / tn);
     kp.gm = t.gm;
-    const size_t osz = (epi == EPI_BF16) ? 2 : 4;
     const uintptr_t align_need = (epi == EPI_BF16) ? 8 : 16;
     bool ov = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(a.out) % align_need == 0);
     if (epi == EPI_BF16) {
         ov = ov && (reinterpret_cast<uintptr_t>(a.sw) % 16 == 0) &&
              (a.bias == nullptr || reinterpret_cast<uintptr_t>(a.bias) % 8 == 0);
     }
-    (void)osz;
     kp.out_vec = ov ? 1 : 0;
-    return t.launch(epi, vec, kp, stream);
+    if (ov && epi == EPI_BF16 && a.N % 8 == 0 && reinterpret_cast<uintptr_t>(a.out) % 16 == 0)
+        kp.out_vec = 2;
+    return vec ? t.launch(epi, kp, stream) : GenericTile::launch(epi, kp, stream);
 }
 
 }  // namespace w8a8
