@@ -17,6 +17,7 @@ Prints one JSON line. Besides the required fields it carries:
   health_gate   bf16 GEMM TFLOP/s of this card (the paper's bf16 health check idea)
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
+       python bench.py --all-shapes           (every workload shape, one JSON line each)
        python bench.py --copy-calibration     (a known-size copy for counter scaling)
 """
 from __future__ import annotations
@@ -349,6 +350,69 @@ def run(args) -> dict:
     return rec
 
 
+def graph_ms(fn, iters: int = 20) -> float:
+    """Mean ms per call of fn, `iters` calls captured in one HIP graph and replayed (no
+    host launch overhead in the measurement, which matters for microsecond shapes)."""
+    import torch
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(iters):
+                fn()
+    g.replay()
+    torch.cuda.synchronize()
+    st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    st.record()
+    for _ in range(3):
+        g.replay()
+    en.record()
+    torch.cuda.synchronize()
+    return st.elapsed_time(en) / (3 * iters)
+
+
+def all_shapes(args):
+    """Every workload shape through the product path (w8a8_linear: per-token quantizer +
+    fused GEMM), plus the fused GEMM alone and bf16 F.linear on the same inputs; one JSON
+    line per shape."""
+    import torch
+    import torch.nn.functional as F
+    import paper_2606_14598_amd as w8a8
+    import synth_inputs as si
+    dev = torch.device("cuda:0")
+    for cfg in sorted(si.WORKLOADS):
+        for shp in si.WORKLOADS[cfg]:
+            x, w, b = si.make_inputs(shp)
+            xd, wd, bd = dev_bf16(x, dev), dev_bf16(w, dev), dev_bf16(b, dev)
+            wq, sw = w8a8.quantize_weight(wd)
+            xq, sx = w8a8.quantize_act(xd)
+            M, N, K = shp.M, shp.N, shp.K
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8,
+                             device=dev)
+            lin = graph_ms(lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws))
+            gem = graph_ms(lambda: w8a8.gemm(xq, sx, wq, sw, bd, out=y))
+            bf = graph_ms(lambda: F.linear(xd, wd, bd))
+            ops = gemm_ops(M, N, K)
+            gb = gemm_bytes(M, N, K)
+            rec = {"config": cfg, "shape": shp.name, "M": M, "K": K, "N": N,
+                   "tile": w8a8.tile_name(w8a8.select_tile(M, N, K)),
+                   "linear_us": round(lin * 1e3, 2), "gemm_us": round(gem * 1e3, 2),
+                   "bf16_linear_us": round(bf * 1e3, 2),
+                   "linear_tops": round(ops / lin / 1e9, 1),
+                   "gemm_tops": round(ops / gem / 1e9, 1),
+                   "gemm_pct_int8_peak": round(100 * ops / gem / 1e9 / PEAK_INT8_TOPS, 2),
+                   "gemm_hbm_GB_s": round(gb / gem / 1e6, 1),
+                   "gemm_pct_hbm": round(100 * gb / gem / 1e6 / PEAK_HBM_GBS, 2),
+                   "bound": "mfma" if ops / gb > PEAK_INT8_TOPS * 1e3 / PEAK_HBM_GBS else "hbm",
+                   "speedup_linear_vs_bf16": round(bf / lin, 3)}
+            print(json.dumps(rec), flush=True)
+            del xd, wd, bd, wq, sw, xq, sx, y, ws
+
+
 def copy_calibration():
     """A plain device copy of known size (for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)."""
     import torch
@@ -372,6 +436,8 @@ def main():
     ap.add_argument("--no-extra", action="store_true",
                     help="only the timed step (health gate, comparators, variant skipped)")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--all-shapes", action="store_true",
+                    help="time every workload shape (one JSON line each)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -383,6 +449,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.all_shapes:
+        all_shapes(args)
         return
     rec = run(args)
     print(json.dumps(rec), flush=True)

@@ -611,6 +611,127 @@ gemm_i8_lds_kernel(KParams kp) {
     store_tile<FN, FM, EPI>(acc, kp, m0 + wm * WTM, n0 + wn * WTN, lane);
 }
 
+// Weight-streaming kernel for few tokens (M <= 16 * FMB): the product is bound by reading
+// W once, so there is no LDS staging of operands. A workgroup owns 16 * FNB output
+// channels and every token; its NW wavefronts take K in super-steps of 256 bytes
+// (super-step j by wavefront j % NW). v_mfma_i32_16x16x64_i8: lane l holds row l % 16 of
+// an operand fragment and K-group l / 16. A dot product is unchanged by any permutation
+// of K applied to both operands alike, so in super-step j lane (r, g) takes bytes
+// [256j + 64s + 16g, +16) of its row for K-step s = 0..3: every load instruction reads
+// whole 64-byte row segments, with the same map for W (rows = channels) and X (rows =
+// tokens). Partial accumulators are summed across wavefronts in LDS (integer, exact),
+// then the epilogue runs as in the tiled kernels: lane l of a 16x16 accumulator holds
+// token l % 16 and channels 4(l / 16) + e.
+template <int FMB, int FNB, int NW, int EPI>
+__global__ void __launch_bounds__(NW * 64)
+gemm_i8_skinny_kernel(KParams kp) {
+    const GemmArgs &a = kp.a;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int r = lane & 15, g = lane >> 4;
+    // Workgroup b: channel block b % tiles_n, token block b / tiles_n (more than one
+    // token block only when more than 16 * FMB tokens are forced onto this kernel).
+    const int64_t n0 = (int64_t)(blockIdx.x % kp.tiles_n) * (16 * FNB);
+    const int64_t mb = (int64_t)(blockIdx.x / kp.tiles_n) * (16 * FMB);
+    const int64_t N = a.N;
+    const int K = (int)a.K;
+    const int rows_w = (int)((N - n0) < 16 * FNB ? (N - n0) : 16 * FNB);
+    const int rows_x = (int)((a.M - mb) < 16 * FMB ? (a.M - mb) : 16 * FMB);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.wq + n0 * K), (short)0, rows_w * K, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.xq + mb * K), (short)0, rows_x * K, kRsrcWord3);
+
+    i32x4 acc[FNB][FMB];
+#pragma unroll
+    for (int c = 0; c < FNB; ++c)
+#pragma unroll
+        for (int b = 0; b < FMB; ++b)
+            acc[c][b] = i32x4{0, 0, 0, 0};
+
+    const int nss = (K + 255) / 256;
+    for (int j = wave; j < nss; j += NW) {
+        const int kb = j * 256 + g * 16;
+        i32x4 wv[FNB][4];
+#pragma unroll
+        for (int c = 0; c < FNB; ++c)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int k = kb + s * 64, row = c * 16 + r;
+                const int off = (k < K && row < rows_w) ? row * K + k : kOOB;
+                wv[c][s] = __builtin_bit_cast(
+                    i32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, 0));
+            }
+#pragma unroll
+        for (int b = 0; b < FMB; ++b) {
+            const int m = b * 16 + r;
+            i32x4 xv[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int k = kb + s * 64;
+                const int off = (k < K && m < rows_x) ? m * K + k : kOOB;
+                xv[s] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+            }
+#pragma unroll
+            for (int c = 0; c < FNB; ++c)
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    acc[c][b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[c][s], xv[s], acc[c][b],
+                                                                     0, 0, 0);
+        }
+    }
+
+    // Cross-wavefront reduction: red[wave][c][b] holds each lane's 4 partial sums.
+    __shared__ i32x4 red[NW][FNB * FMB][64];
+#pragma unroll
+    for (int c = 0; c < FNB; ++c)
+#pragma unroll
+        for (int b = 0; b < FMB; ++b)
+            red[wave][c * FMB + b][lane] = acc[c][b];
+    __syncthreads();
+    for (int cb = wave; cb < FNB * FMB; cb += NW) {
+        const int c = cb / FMB, b = cb % FMB;
+        i32x4 t = red[0][cb][lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w)
+            t += red[w][cb][lane];
+        const int64_t n = n0 + c * 16 + g * 4;
+        if (b * 16 + r >= rows_x || n >= N)
+            continue;
+        const int64_t m = mb + b * 16 + r;
+        if constexpr (EPI == EPI_I32) {
+            int32_t *o = static_cast<int32_t *>(a.out) + m * N + n;
+            if (kp.out_vec && n + 3 < N) {
+                *reinterpret_cast<i32x4 *>(o) = t;
+            } else {
+                for (int e = 0; e < 4 && n + e < N; ++e)
+                    o[e] = t[e];
+            }
+        } else {
+            uint16_t *o = static_cast<uint16_t *>(a.out) + m * N + n;
+            const float sxm = a.sx[m];
+            uint16_t hv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (n + e < N) {
+                    const float bb = a.bias ? __uint_as_float((uint32_t)a.bias[n + e] << 16) : 0.0f;
+                    const float y = __builtin_fmaf((float)t[e], sxm * a.sw[n + e], bb);
+                    hv[e] = __builtin_bit_cast(uint16_t, (__bf16)y);
+                }
+            }
+            if (kp.out_vec && n + 3 < N) {
+                uint2 pk;
+                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                *reinterpret_cast<uint2 *>(o) = pk;
+            } else {
+                for (int e = 0; e < 4 && n + e < N; ++e)
+                    o[e] = hv[e];
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- tile registry
 
 template <int TM, int TN, int BK, int WM, int WN, int S>
@@ -636,6 +757,21 @@ struct Tile {
             else
                 hipLaunchKernelGGL((gemm_i8_kernel<TM, TN, BK, WM, WN, true, EPI_I32>), grid, block, 0, s, kp);
         }
+        return hipGetLastError();
+    }
+};
+
+// Few tokens: the weight-streaming kernel (one workgroup per 16 channels).
+template <int FMB, int FNB, int NW>
+struct SkinnyTile {
+    static constexpr int threads = NW * 64;
+    static constexpr int lds = NW * FNB * FMB * 64 * 16;
+    static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
+        const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n)), block(threads);
+        if (epi == EPI_BF16)
+            hipLaunchKernelGGL((gemm_i8_skinny_kernel<FMB, FNB, NW, EPI_BF16>), grid, block, 0, s, kp);
+        else
+            hipLaunchKernelGGL((gemm_i8_skinny_kernel<FMB, FNB, NW, EPI_I32>), grid, block, 0, s, kp);
         return hipGetLastError();
     }
 };
@@ -666,7 +802,15 @@ struct TileEntry {
             GM, &Tile<TM, TN, BK, WM, WN, S>::launch                                         \
     }
 
-// Names: m<TM>n<TN>k<BK>w<WM>x<WN>[s<S>]; "s<S>" = direct-to-LDS pipelined kernel with S
+#define W8A8_SKINNY(NAME, FMB, FNB, NW)                                                  \
+    TileEntry {                                                                              \
+        {NAME, 16 * FMB, 16 * FNB, 256, SkinnyTile<FMB, FNB, NW>::threads,                  \
+         SkinnyTile<FMB, FNB, NW>::lds},                                                     \
+            1, &SkinnyTile<FMB, FNB, NW>::launch                                             \
+    }
+
+// Names: m<TM>n<TN>k<BK>w<WM>x<WN>[s<S>]; skinny_m<Mmax>n<C>w<NW> = weight-streaming
+// kernel for at most Mmax tokens, C channels per workgroup. "s<S>" = direct-to-LDS pipelined kernel with S
 // stages (used when the operands are 16-byte aligned and K % 16 == 0; otherwise the
 // register-staged kernel of the same tile runs).
 const TileEntry kTiles[] = {
@@ -685,6 +829,11 @@ const TileEntry kTiles[] = {
     W8A8_TILE("m64n128k128w1x4", 64, 128, 128, 1, 4, 8, 0),
     W8A8_TILE("m32n128k128w1x4", 32, 128, 128, 1, 4, 8, 0),
     W8A8_TILE("m32n64k128w1x2", 32, 64, 128, 1, 2, 8, 0),
+    W8A8_SKINNY("skinny_m16n16w16", 1, 1, 16),
+    W8A8_SKINNY("skinny_m32n16w16", 2, 1, 16),
+    W8A8_SKINNY("skinny_m16n64w16", 1, 4, 16),
+    W8A8_SKINNY("skinny_m64n32w16", 4, 2, 16),
+    W8A8_SKINNY("skinny_m128n32w8", 8, 2, 8),
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -706,10 +855,15 @@ int fallback_tile(int64_t M, int64_t N, int64_t K) {
         if (tiles >= cus)
             return id;
     }
+    // Few tokens: stream the weight (one workgroup per 16 channels).
+    if (M <= 16)
+        return N >= 256 * 64 ? 17 : 15;
     if (M <= 32)
-        return 14;
+        return 16;
     if (M <= 64)
-        return 13;
+        return 18;
+    if (M <= 128)
+        return 19;
     return 12;
 }
 
