@@ -8,8 +8,9 @@
 //
 // The kernel is HBM-bound (3 bytes moved per element: 2 read, 1 written). Rows whose
 // K fits the register file are read once with 16-byte loads, kept in VGPRs for the
-// second (quantizing) pass and written with 8-byte stores; the row maximum is taken on
-// the bf16 bit patterns (|v| ordered as an unsigned integer, exact for finite values)
+// second (quantizing) pass and written with 8-byte stores, by a persistent grid that
+// prefetches the next rows while it finishes the current ones; the row maximum is taken
+// on the bf16 bit patterns (|v| ordered as an unsigned integer, exact for finite values)
 // with a wavefront butterfly and, for 256-thread rows, one LDS exchange.
 #include "w8a8_internal.hpp"
 
@@ -79,50 +80,74 @@ __device__ __forceinline__ RowScale row_scale(uint32_t amax_bits) {
     return r;
 }
 
-// Register-resident path: TPR threads per row (64 = one wavefront, 256 = the block),
-// NV 16-byte vectors per thread, K % 8 == 0, v 16-byte and q 8-byte aligned.
+// Register-resident path, persistent and software-pipelined: TPR threads per row
+// (64 = one wavefront, 256 = the block), NV 16-byte vectors per thread (K % 8 == 0,
+// v 16-byte and q 8-byte aligned). Row group j of a block holds rows j*RPB .. j*RPB +
+// RPB - 1; block b handles row groups b, b + G, b + 2G, ... (G = gridDim.x) and loads
+// group j + G while it reduces, quantizes and stores group j, so the HBM reads of the
+// next rows overlap the work and the stores of the current ones.
 template <int TPR, int NV>
 __global__ void __launch_bounds__(256)
 quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
                int8_t *__restrict__ q, float *__restrict__ scale) {
     constexpr int RPB = 256 / TPR;
     const int t = threadIdx.x % TPR;
-    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;
-    const bool live = row < rows;
+    const int sub = threadIdx.x / TPR;
     const int64_t nvec = K >> 3;
-    const uint4 *src = reinterpret_cast<const uint4 *>(v + (live ? row : 0) * K);
+    const int64_t groups = (rows + RPB - 1) / RPB;
+    __shared__ uint32_t part[RPB][TPR / 64];
 
-    uint4 d[NV];
-    uint32_t m = 0;
+    auto load = [&](uint4 (&d)[NV], int64_t grp) {
+        const int64_t row = grp * RPB + sub;
+        const bool live = grp < groups && row < rows;
+        const uint4 *src = reinterpret_cast<const uint4 *>(v + (live ? row : 0) * K);
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int64_t vi = (int64_t)j * TPR + t;
-        if (live && vi < nvec) {
-            d[j] = src[vi];
-        } else {
-            d[j] = make_uint4(0, 0, 0, 0);
+        for (int j = 0; j < NV; ++j) {
+            const int64_t vi = (int64_t)j * TPR + t;
+            if (live && vi < nvec)
+                d[j] = src[vi];
+            else
+                d[j] = make_uint4(0, 0, 0, 0);
         }
-        m = max(m, absmax8(d[j]));
-    }
-    m = wave_max(m);
-    if constexpr (TPR == 256) {
-        __shared__ uint32_t part[4];
-        if ((threadIdx.x & 63) == 0)
-            part[threadIdx.x >> 6] = m;
-        __syncthreads();
-        m = max(max(part[0], part[1]), max(part[2], part[3]));
-    }
-    const RowScale rs = row_scale(m);
-    if (!live)
-        return;
-    if (t == 0)
-        scale[row] = rs.scale;
-    uint2 *dst = reinterpret_cast<uint2 *>(q + row * K);
+    };
+    auto process = [&](const uint4 (&d)[NV], int64_t grp) {
+        const int64_t row = grp * RPB + sub;
+        uint32_t m = 0;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int64_t vi = (int64_t)j * TPR + t;
-        if (vi < nvec)
-            dst[vi] = code8(d[j], rs.inv);
+        for (int j = 0; j < NV; ++j)
+            m = max(m, absmax8(d[j]));
+        m = wave_max(m);
+        if constexpr (TPR == 256) {
+            if ((threadIdx.x & 63) == 0)
+                part[sub][(threadIdx.x >> 6) & 3] = m;
+            __syncthreads();
+            m = max(max(part[sub][0], part[sub][1]), max(part[sub][2], part[sub][3]));
+            __syncthreads();   // part is rewritten by the next row group
+        }
+        const RowScale rs = row_scale(m);
+        if (row >= rows)
+            return;
+        if (t == 0)
+            scale[row] = rs.scale;
+        uint2 *dst = reinterpret_cast<uint2 *>(q + row * K);
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int64_t vi = (int64_t)j * TPR + t;
+            if (vi < nvec)
+                dst[vi] = code8(d[j], rs.inv);
+        }
+    };
+
+    uint4 a[NV], b[NV];
+    int64_t grp = blockIdx.x;
+    load(a, grp);
+    for (; grp < groups; grp += 2 * (int64_t)gridDim.x) {
+        load(b, grp + gridDim.x);
+        process(a, grp);
+        if (grp + gridDim.x >= groups)
+            break;
+        load(a, grp + 2 * (int64_t)gridDim.x);
+        process(b, grp + gridDim.x);
     }
 }
 
@@ -171,7 +196,10 @@ template <int TPR, int NV>
 hipError_t launch_reg(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
                       float *scale, hipStream_t s) {
     constexpr int RPB = 256 / TPR;
-    const int64_t blocks = (rows + RPB - 1) / RPB;
+    const int64_t groups = (rows + RPB - 1) / RPB;
+    // Persistent grid: a few blocks per CU, each walking row groups with prefetch.
+    const int64_t max_blocks = 256 * 8;
+    const int64_t blocks = groups < max_blocks ? groups : max_blocks;
     hipLaunchKernelGGL((quant_rows_reg<TPR, NV>), dim3((unsigned)blocks), dim3(256), 0, s,
                        v, rows, K, q, scale);
     return hipGetLastError();
