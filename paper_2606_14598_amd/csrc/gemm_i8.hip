@@ -492,43 +492,42 @@ gemm_i8_lds_kernel(KParams kp) {
             fb[buf][j] = *reinterpret_cast<const i32x4 *>(sx_ + j * 32 * BK);
     };
 
-    // Each K-step runs as G fenced groups: a slice of the next K-step's fragment reads and
-    // of the loads of panel k+S-1, then a slice of this K-step's MFMAs. The matrix core
-    // thus always has MFMAs queued while the memory instructions issue, and the reads
-    // have the rest of the K-step to land.
+    // Each K-step interleaves its memory instructions one by one with its MFMAs: the
+    // ds_reads of the next K-step's fragments first (they must land within this step),
+    // then its share of the loads of panel k+S-1, each followed by one MFMA, with a
+    // scheduling fence around every pair. The matrix core then always has an MFMA
+    // queued while a memory instruction issues.
     constexpr int NM = FN * FM, NR = FN + FM;
     constexpr int VPS = (NV + KS - 1) / KS;   // loads per K-step
-    constexpr int G = NM >= 4 ? 4 : NM;       // groups per K-step
     auto kstep = [&](auto ksc, int so, int kt_load, int so_load) {
         constexpr int ks = decltype(ksc)::value;
-        [&]<int... g>(std::integer_sequence<int, g...>) {
+        constexpr int nr = ks + 1 < KS ? NR : 0;
+        constexpr int va = ks * VPS < NV ? ks * VPS : NV;
+        constexpr int vb = (ks + 1) * VPS < NV ? (ks + 1) * VPS : NV;
+        constexpr int nops = nr + (vb - va);
+        constexpr int steps = NM > nops ? NM : nops;
+        const int8_t *sw_ = smem + so + wn * WTN * BK + fofs[ks + 1 < KS ? ks + 1 : 0];
+        const int8_t *sx_ = smem + so + TN * BK + wm * WTM * BK + fofs[ks + 1 < KS ? ks + 1 : 0];
+        [&]<int... q>(std::integer_sequence<int, q...>) {
             ([&] {
-                if constexpr (ks + 1 < KS) {
-                    const int8_t *sw_ = smem + so + wn * WTN * BK + fofs[ks + 1];
-                    const int8_t *sx_ = smem + so + TN * BK + wm * WTM * BK + fofs[ks + 1];
-                    constexpr int r0_ = g * NR / G, r1_ = (g + 1) * NR / G;
-#pragma unroll
-                    for (int r = r0_; r < r1_; ++r) {
-                        if (r < FN)
-                            fa[(ks + 1) & 1][r] = *reinterpret_cast<const i32x4 *>(sw_ + r * 32 * BK);
-                        else
-                            fb[(ks + 1) & 1][r - FN] =
-                                *reinterpret_cast<const i32x4 *>(sx_ + (r - FN) * 32 * BK);
-                    }
+                if constexpr (q < nr) {
+                    if constexpr (q < FN)
+                        fa[(ks + 1) & 1][q] = *reinterpret_cast<const i32x4 *>(sw_ + q * 32 * BK);
+                    else
+                        fb[(ks + 1) & 1][q - FN] =
+                            *reinterpret_cast<const i32x4 *>(sx_ + (q - FN) * 32 * BK);
+                } else if constexpr (q < nops) {
+                    issue(std::integral_constant<int, va + q - nr>{},
+                          std::integral_constant<int, va + q - nr + 1>{}, kt_load, so_load);
                 }
-                constexpr int va = ks * VPS + g * VPS / G, vb = ks * VPS + (g + 1) * VPS / G;
-                constexpr int v0 = va < NV ? va : NV, v1 = vb < NV ? vb : NV;
-                issue(std::integral_constant<int, v0>{}, std::integral_constant<int, v1>{}, kt_load,
-                      so_load);
-                __builtin_amdgcn_sched_barrier(0);
-                constexpr int q0 = g * NM / G, q1 = (g + 1) * NM / G;
-#pragma unroll
-                for (int q = q0; q < q1; ++q)
+                if constexpr (q < NM) {
+                    __builtin_amdgcn_sched_barrier(0);
                     acc[q / FM][q % FM] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
                         fa[ks & 1][q / FM], fb[ks & 1][q % FM], acc[q / FM][q % FM], 0, 0, 0);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }(), ...);
-        }(std::make_integer_sequence<int, G>{});
+        }(std::make_integer_sequence<int, steps>{});
     };
 
     // Tile vectors for the epilogue: fetched now, parked in LDS after the prologue (their
