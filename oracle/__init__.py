@@ -15,6 +15,12 @@ recipe (reused)" and "The fused kernel"):
   epilogue(acc, sx, sw, b_bits)    bf16(fmaf(float(acc), sx*sw, b))
   epilogue_f64(...)                diagnostic: same in double, rounded once
   linear(x_bits, wq, sw, b_bits)   quantize X per token, product, epilogue
+  quantize_rows(v_bits, act=, col_mul=)
+                                   the row rule on T(x) * c[k] (T identity or GELU,
+                                   c the SmoothQuant runtime multiplier)
+  gelu_f64(x)                      x * Phi(x) in double (via erfc)
+  col_absmax(v_bits, act=)         per-column max |T(x)| (calibration)
+  smooth_factors(ax, aw, alpha)    SmoothQuant factors s and 1/s per input channel
 """
 from __future__ import annotations
 
@@ -60,6 +66,10 @@ def _load():
     I64 = ctypes.c_int64
     INT = ctypes.c_int
     lib.orc_quantize_rows.argtypes = [P, I64, I64, P, P, INT]
+    lib.orc_quantize_rows_ex.argtypes = [P, I64, I64, INT, P, P, P, INT]
+    lib.orc_col_absmax.argtypes = [P, I64, I64, INT, P]
+    lib.orc_smooth_factors.argtypes = [P, P, I64, ctypes.c_float, P, P]
+    lib.orc_gelu_f64_array.argtypes = [P, I64, P]
     lib.orc_gemm_acc.argtypes = [P, P, I64, I64, I64, P, INT]
     lib.orc_epilogue.argtypes = [P, P, P, P, I64, I64, P, INT]
     lib.orc_epilogue_f64.argtypes = [P, P, P, P, I64, I64, P, INT]
@@ -74,7 +84,7 @@ def _load():
     lib.orc_f32_to_bf16_array.argtypes = [P, I64, P]
     lib.orc_f64_to_bf16_array.argtypes = [P, I64, P]
     for f in ("orc_quantize_rows", "orc_gemm_acc", "orc_epilogue", "orc_epilogue_f64",
-              "orc_linear"):
+              "orc_linear", "orc_quantize_rows_ex", "orc_col_absmax", "orc_smooth_factors"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -120,14 +130,55 @@ def bf16_to_f32(bits) -> np.ndarray:
     return (b.astype(np.uint32) << 16).view(np.float32)
 
 
-def quantize_rows(v_bits, nthreads: int = 0):
-    """Per-row absmax quantization: returns (q int8 [R,K], scale float32 [R])."""
+ACTS = {"none": 0, "gelu": 1}
+
+
+def quantize_rows(v_bits, nthreads: int = 0, *, act: str = "none", col_mul=None):
+    """Per-row absmax quantization of v = T(x) * col_mul[k]: returns (q int8 [R,K],
+    scale float32 [R]). act "none" is the plain rule on the bf16 values."""
     v = _c(v_bits, np.uint16)
     R, K = v.shape
     q = np.empty((R, K), np.int8)
     s = np.empty(R, np.float32)
-    _check(_load().orc_quantize_rows(_ptr(v), R, K, _ptr(q), _ptr(s), nthreads))
+    if act == "none" and col_mul is None:
+        _check(_load().orc_quantize_rows(_ptr(v), R, K, _ptr(q), _ptr(s), nthreads))
+        return q, s
+    cm = None if col_mul is None else _c(col_mul, np.float32)
+    if cm is not None and cm.shape != (K,):
+        raise ValueError("col_mul must be [K]")
+    _check(_load().orc_quantize_rows_ex(_ptr(v), R, K, ACTS[act], _ptr(cm), _ptr(q), _ptr(s),
+                                        nthreads))
     return q, s
+
+
+def gelu_f64(x) -> np.ndarray:
+    """GELU(x) = x * Phi(x) in double precision."""
+    v = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty_like(v)
+    _load().orc_gelu_f64_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def col_absmax(v_bits, *, act: str = "none") -> np.ndarray:
+    """amax[k] = max_r |T(x[r, k])| as float32."""
+    v = _c(v_bits, np.uint16)
+    R, K = v.shape
+    out = np.empty(K, np.float32)
+    _check(_load().orc_col_absmax(_ptr(v), R, K, ACTS[act], _ptr(out)))
+    return out
+
+
+def smooth_factors(ax, aw, alpha: float = 0.5):
+    """SmoothQuant factors: (s, s_inv) float32 [K], s = ax^alpha / aw^(1 - alpha)."""
+    ax = _c(ax, np.float32)
+    aw = _c(aw, np.float32)
+    if ax.shape != aw.shape or ax.ndim != 1:
+        raise ValueError("ax and aw must be matching [K] vectors")
+    s = np.empty_like(ax)
+    si = np.empty_like(ax)
+    _check(_load().orc_smooth_factors(_ptr(ax), _ptr(aw), ax.size, float(alpha), _ptr(s),
+                                      _ptr(si)))
+    return s, si
 
 
 def gemm_acc(xq, wq, nthreads: int = 0):

@@ -18,6 +18,16 @@
  *     epilogue works directly on the accumulator and emits the dequantized result).
  *   - orc_epilogue_f64: diagnostic only; the same dequantization in double, rounded
  *     once to bf16, to show how far the float32 epilogue is from the exact value.
+ *   - orc_quantize_rows_ex: the same row rule applied to transformed values
+ *     v[k] = T(x[k]) * c[k]: T the identity or the exact (erf) GELU, c an optional
+ *     per-K-channel multiplier. The multiplier is the runtime half of SmoothQuant
+ *     (Section 3, "The quantization recipe (reused)": SmoothQuant with alpha = 0.5):
+ *     X is divided per input channel by the smoothing factor, W multiplied by it, so
+ *     the product is unchanged. GELU in front of the quantizer is the activation that
+ *     feeds the MLP down-projection of the DiT (Section 3, "Target architecture").
+ *   - orc_col_absmax, orc_smooth_factors: offline calibration of the smoothing
+ *     factors, s[k] = max|X[:,k]|^alpha / max|W[:,k]|^(1 - alpha), the published
+ *     SmoothQuant rule the recipe names.
  *
  * The paper leaves the following open; these readings are fixed here and bind the GPU
  * path too:
@@ -30,7 +40,16 @@
  *   - epilogue: y = bf16_rne(fmaf((float)acc, sx[m] * sw[n], b[n])), b = +0 when there
  *     is no bias, (float)acc rounded to nearest even;
  *   - inputs must be finite (the paper's gate is "no NaNs"); a non-finite input is
- *     rejected with an error code.
+ *     rejected with an error code;
+ *   - transformed rows: t = GELU(x) is the double-precision value
+ *     0.5 * x * erfc(-x / sqrt(2)) rounded once to float32 (the GPU computes its own
+ *     float32 GELU, equal to this within a few units in the last place); v = t * c[k]
+ *     is one float32 multiply; a = max |v|, and the row rule above applies to v;
+ *   - smoothing factors: alpha = 0.5 gives s = sqrtf(ax) / sqrtf(aw) (each operation
+ *     correctly rounded float32, so both sides agree bit for bit); any other alpha
+ *     gives the double-precision value ax^alpha / aw^(1 - alpha) rounded to float32;
+ *     a channel with ax or aw zero, or a factor that is zero or not finite, gets
+ *     s = 1 (left unsmoothed); the runtime multiplier is s_inv = 1.0f / s.
  *
  * Build: gcc -O2 -std=c11 -ffp-contract=off -fopenmp (no implicit FMA contraction, so
  * every float operation is exactly the one written).
@@ -106,12 +125,41 @@ int orc_max_threads(void)
 #endif
 }
 
-/* Per-row symmetric absmax quantization (Section 3, "The quantization recipe
- * (reused)"). v: [rows, K] bf16 bits, row-major. q: [rows, K] int8. scale: [rows]. */
-int orc_quantize_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
-                      float *scale, int nthreads)
+/* Exact (to double precision) GELU: x * Phi(x), written with erfc so that the left
+ * tail keeps its relative accuracy (1 + erf(z) would cancel for z << 0). */
+static double gelu_f64(double x)
 {
-    if (rows < 0 || K < 0)
+    return 0.5 * x * erfc(-x / sqrt(2.0));
+}
+
+void orc_gelu_f64_array(const double *x, int64_t n, double *out)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = gelu_f64(x[i]);
+}
+
+#define ORC_ACT_NONE 0
+#define ORC_ACT_GELU 1
+
+/* The value the row rule sees for element k: T(x) as float32, times c[k] if given. */
+static float transformed(uint16_t h, int act, const float *colmul, int64_t k)
+{
+    float t = bf16_bits_to_f32(h);
+    if (act == ORC_ACT_GELU)
+        t = (float)gelu_f64((double)t);
+    if (colmul)
+        t = t * colmul[k];          /* one float32 multiply */
+    return t;
+}
+
+/* Per-row symmetric absmax quantization (Section 3, "The quantization recipe
+ * (reused)") of the transformed values v[k] = T(x[k]) * c[k]. x: [rows, K] bf16 bits,
+ * row-major. act: 0 identity, 1 GELU. colmul: [K] or NULL. q: [rows, K] int8.
+ * scale: [rows]. */
+int orc_quantize_rows_ex(const uint16_t *x, int64_t rows, int64_t K, int act,
+                         const float *colmul, int8_t *q, float *scale, int nthreads)
+{
+    if (rows < 0 || K < 0 || (act != ORC_ACT_NONE && act != ORC_ACT_GELU))
         return ORC_ERR_ARG;
     if (fegetround() != FE_TONEAREST)
         return ORC_ERR_ROUNDING_MODE;
@@ -119,18 +167,20 @@ int orc_quantize_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
     set_threads(nthreads);
 #pragma omp parallel for schedule(static)
     for (int64_t r = 0; r < rows; ++r) {
-        const uint16_t *row = v + r * K;
+        const uint16_t *row = x + r * K;
         int8_t *qrow = q + r * K;
-        /* a = max_k |v[k]|: exact, since bf16 -> float32 is exact. */
+        /* a = max_k |v[k]|; for the identity transform v is the bf16 value, exact. */
         float a = 0.0f;
         int finite = 1;
         for (int64_t k = 0; k < K; ++k) {
-            float x = bf16_bits_to_f32(row[k]);
-            if (!isfinite(x))
+            if (!isfinite(bf16_bits_to_f32(row[k])))
                 finite = 0;
-            float ax = fabsf(x);
-            if (ax > a)
-                a = ax;
+            float v = transformed(row[k], act, colmul, k);
+            if (!isfinite(v))
+                finite = 0;
+            float av = fabsf(v);
+            if (av > a)
+                a = av;
         }
         if (!finite) {
 #pragma omp atomic write
@@ -147,8 +197,8 @@ int orc_quantize_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
         }
         scale[r] = s;
         for (int64_t k = 0; k < K; ++k) {
-            float p = bf16_bits_to_f32(row[k]) * inv;   /* one float32 multiply */
-            float n = nearbyintf(p);                    /* ties to even */
+            float p = transformed(row[k], act, colmul, k) * inv;   /* one float32 multiply */
+            float n = nearbyintf(p);                               /* ties to even */
             if (n > 127.0f)
                 n = 127.0f;
             if (n < -127.0f)
@@ -157,6 +207,55 @@ int orc_quantize_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
         }
     }
     return err;
+}
+
+/* The plain rule: identity transform, no multiplier. */
+int orc_quantize_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
+                      float *scale, int nthreads)
+{
+    return orc_quantize_rows_ex(v, rows, K, ORC_ACT_NONE, NULL, q, scale, nthreads);
+}
+
+/* Calibration: amax[k] = max over rows of |T(x[r][k])| (float32, T as above). */
+int orc_col_absmax(const uint16_t *x, int64_t rows, int64_t K, int act, float *amax)
+{
+    if (rows < 0 || K < 0 || (act != ORC_ACT_NONE && act != ORC_ACT_GELU))
+        return ORC_ERR_ARG;
+    for (int64_t k = 0; k < K; ++k)
+        amax[k] = 0.0f;
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int64_t k = 0; k < K; ++k) {
+            if (!isfinite(bf16_bits_to_f32(x[r * K + k])))
+                return ORC_ERR_NONFINITE;
+            float v = fabsf(transformed(x[r * K + k], act, NULL, k));
+            if (v > amax[k])
+                amax[k] = v;
+        }
+    }
+    return ORC_OK;
+}
+
+/* SmoothQuant factors from calibrated per-channel maxima of X and of W. */
+int orc_smooth_factors(const float *ax, const float *aw, int64_t K, float alpha,
+                       float *s, float *s_inv)
+{
+    if (K < 0 || !(alpha >= 0.0f && alpha <= 1.0f))
+        return ORC_ERR_ARG;
+    for (int64_t k = 0; k < K; ++k) {
+        float a = ax[k], b = aw[k];
+        float f = 1.0f;
+        if (a > 0.0f && b > 0.0f && isfinite(a) && isfinite(b)) {
+            if (alpha == 0.5f)
+                f = sqrtf(a) / sqrtf(b);
+            else
+                f = (float)(pow((double)a, (double)alpha) / pow((double)b, 1.0 - (double)alpha));
+            if (!(f > 0.0f) || !isfinite(f))
+                f = 1.0f;
+        }
+        s[k] = f;
+        s_inv[k] = 1.0f / f;
+    }
+    return ORC_OK;
 }
 
 /* Exact integer product (Section 3, "The fused kernel": int8 x int8 -> int32).
