@@ -118,6 +118,64 @@ w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *ac
                                  int64_t M, int64_t N, int64_t K, int tile_id,
                                  void *stream);
 
+/* ---- Transformed activations and SmoothQuant (Section 3, "The quantization recipe
+ * (reused)": per-channel int8 weights, per-token dynamic int8 activations, and
+ * SmoothQuant with alpha = 0.5).
+ *
+ * SmoothQuant moves quantization difficulty from activations to weights per input
+ * channel k: X is multiplied by smooth_inv[k] = 1 / s[k] and W by s[k], which leaves
+ * X W^T unchanged, with s[k] = max|X[:,k]|^alpha / max|W[:,k]|^(1 - alpha) calibrated
+ * offline. The weight side is folded once (w8a8_quantize_weight_ex); the activation
+ * side is a multiply inside the per-token quantizer, so it costs no pass over X.
+ *
+ * act selects a transform T applied to the bf16 input before the multiplier:
+ *   W8A8_ACT_NONE  T(x) = x
+ *   W8A8_ACT_GELU  T(x) = x * Phi(x), the exact (erf) GELU, evaluated in float32 to
+ *                  within a few units in the last place of the exact value. It feeds
+ *                  the MLP down-projection from the pre-activation, with no GELU pass
+ *                  of its own.
+ * The quantizer then applies the row rule above to v[k] = T(x[k]) * col_mul[k]
+ * (float32 multiply; col_mul NULL means no multiplier). Any other act value returns
+ * W8A8_ERR_ARG. */
+#define W8A8_ACT_NONE 0
+#define W8A8_ACT_GELU 1
+
+/* Per-token quantization of T(x) * col_mul. x: [M,K] bf16; col_mul: [K] float32 or
+ * NULL. Out: xq [M,K] int8, x_scale [M] float32. */
+w8a8_status w8a8_quantize_act_ex(const uint16_t *x, int64_t M, int64_t K, int act,
+                                 const float *col_mul, int8_t *xq, float *x_scale,
+                                 void *stream);
+
+/* Per-output-channel quantization of w[n][k] * col_mul[k] (the SmoothQuant fold; col_mul
+ * = s, or NULL for the plain rule). w: [N,K] bf16. Out: wq [N,K], w_scale [N]. */
+w8a8_status w8a8_quantize_weight_ex(const uint16_t *w, int64_t N, int64_t K,
+                                    const float *col_mul, int8_t *wq, float *w_scale,
+                                    void *stream);
+
+/* w8a8_linear on T(x) * col_mul: for a smoothed layer col_mul = smooth_inv and wq was
+ * quantized with col_mul = smooth. Same workspace as w8a8_linear. */
+w8a8_status w8a8_linear_ex(const uint16_t *x, int act, const float *col_mul,
+                           const int8_t *wq, const float *w_scale, const uint16_t *bias,
+                           uint16_t *y, int64_t M, int64_t N, int64_t K, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+/* Calibration: amax[k] = max over the R rows of |T(v[r][k])| (float32). With
+ * accumulate != 0 the result is merged (max) into amax's current contents, so several
+ * calibration batches can be folded in; otherwise amax is overwritten. v: [R,K] bf16
+ * (activations, or W itself for the weight maxima). amax: [K] float32. */
+w8a8_status w8a8_col_absmax(const uint16_t *v, int64_t R, int64_t K, int act, float *amax,
+                            int accumulate, void *stream);
+
+/* SmoothQuant factors from calibrated maxima: smooth[k] = x_amax^alpha /
+ * w_amax^(1 - alpha), smooth_inv[k] = 1.0f / smooth[k]. alpha = 0.5 (the recipe's
+ * value) computes sqrtf(x_amax) / sqrtf(w_amax), each step correctly rounded; other
+ * alpha use powf. A channel whose maxima are not both positive and finite, or whose
+ * factor is 0 or infinite, gets smooth = 1. alpha outside [0, 1] returns
+ * W8A8_ERR_ARG. All arrays [K] float32 on the device. */
+w8a8_status w8a8_smooth_factors(const float *x_amax, const float *w_amax, int64_t K,
+                                float alpha, float *smooth, float *smooth_inv,
+                                void *stream);
+
 /* Static description of a status code. */
 const char *w8a8_status_string(w8a8_status status);
 

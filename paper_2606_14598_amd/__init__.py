@@ -9,6 +9,12 @@ current HIP stream through ctypes. Entry points mirror the C ABI in include/w8a8
   gemm(xq, x_scale, wq, w_scale, b)  -> y bf16 [M,N]
   linear(x, wq, w_scale, b)          -> y bf16 [..., N]   (x [..., K])
   gemm_acc_i32(xq, wq)               -> acc int32 [M,N]   (debug, no epilogue)
+  col_absmax(v, act=)                -> amax fp32 [K]     (calibration)
+  smooth_factors(x_amax, w_amax)     -> (s, s_inv) fp32 [K] (SmoothQuant, alpha = 0.5)
+
+quantize_act and linear take act="gelu" (quantize GELU(x), exact erf, instead of x) and
+col_mul (a per-input-channel float32 multiplier: SmoothQuant's 1/s); quantize_weight
+takes col_mul (SmoothQuant's s, folded into W before quantization).
 
 The method is Section 3 of the paper ("The quantization recipe (reused)", "The fused
 kernel"): per-channel int8 weights, per-token dynamic int8 activations, an int8 x int8
@@ -23,6 +29,7 @@ import os
 import torch
 
 __all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
+           "col_absmax", "smooth_factors", "ACTS",
            "tile_count", "tile_name", "select_tile", "gemm_workspace_bytes",
            "linear_workspace_bytes", "library_path", "load_library", "W8A8Error",
            "MAX_K", "version"]
@@ -58,6 +65,11 @@ def load_library():
     sigs = {
         "w8a8_quantize_weight": ([P, I64, I64, P, P, P], INT),
         "w8a8_quantize_act": ([P, I64, I64, P, P, P], INT),
+        "w8a8_quantize_weight_ex": ([P, I64, I64, P, P, P, P], INT),
+        "w8a8_quantize_act_ex": ([P, I64, I64, INT, P, P, P, P], INT),
+        "w8a8_linear_ex": ([P, INT, P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
+        "w8a8_col_absmax": ([P, I64, I64, INT, P, INT, P], INT),
+        "w8a8_smooth_factors": ([P, P, I64, ctypes.c_float, P, P, P], INT),
         "w8a8_gemm": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
         "w8a8_gemm_ex": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, INT, P], INT),
         "w8a8_gemm_workspace_bytes": ([I64, I64, I64], SZ),
@@ -140,24 +152,88 @@ def linear_workspace_bytes(M: int, N: int, K: int) -> int:
     return int(load_library().w8a8_linear_workspace_bytes(M, N, K))
 
 
-def _quantize(fn: str, v: torch.Tensor, name: str):
-    _check(v, torch.bfloat16, 2, name)
-    R, K = v.shape
-    q = torch.empty((R, K), dtype=torch.int8, device=v.device)
-    s = torch.empty((R,), dtype=torch.float32, device=v.device)
-    with torch.cuda.device(v.device):
-        _call(fn, _ptr(v), R, K, _ptr(q), _ptr(s), _stream(v.device))
+ACTS = {"none": 0, "gelu": 1}
+
+
+def _act(act: str) -> int:
+    if act not in ACTS:
+        raise ValueError(f"act must be one of {sorted(ACTS)}, got {act!r}")
+    return ACTS[act]
+
+
+def _col_mul(col_mul, K: int, device):
+    if col_mul is None:
+        return None
+    _check(col_mul, torch.float32, 1, "col_mul")
+    if col_mul.shape[0] != K:
+        raise ValueError(f"col_mul must have K={K} entries, got {col_mul.shape[0]}")
+    if col_mul.device != torch.device(device):
+        raise ValueError(f"col_mul is on {col_mul.device}, expected {device}")
+    return col_mul
+
+
+def quantize_weight(w: torch.Tensor, *, col_mul=None):
+    """Per-output-channel int8 weights: w bf16 [N,K] -> (wq int8 [N,K], sw fp32 [N]).
+    col_mul: optional fp32 [K] multiplier (the SmoothQuant factors s)."""
+    _check(w, torch.bfloat16, 2, "w")
+    N, K = w.shape
+    cm = _col_mul(col_mul, K, w.device)
+    q = torch.empty((N, K), dtype=torch.int8, device=w.device)
+    s = torch.empty((N,), dtype=torch.float32, device=w.device)
+    with torch.cuda.device(w.device):
+        _call("w8a8_quantize_weight_ex", _ptr(w), N, K, _ptr(cm), _ptr(q), _ptr(s),
+              _stream(w.device))
     return q, s
 
 
-def quantize_weight(w: torch.Tensor):
-    """Per-output-channel int8 weights: w bf16 [N,K] -> (wq int8 [N,K], sw fp32 [N])."""
-    return _quantize("w8a8_quantize_weight", w, "w")
+def quantize_act(x: torch.Tensor, *, act: str = "none", col_mul=None):
+    """Per-token int8 activations: x bf16 [M,K] -> (xq int8 [M,K], sx fp32 [M]) of
+    T(x) * col_mul (T = identity or GELU)."""
+    a = _act(act)
+    _check(x, torch.bfloat16, 2, "x")
+    M, K = x.shape
+    cm = _col_mul(col_mul, K, x.device)
+    q = torch.empty((M, K), dtype=torch.int8, device=x.device)
+    s = torch.empty((M,), dtype=torch.float32, device=x.device)
+    with torch.cuda.device(x.device):
+        _call("w8a8_quantize_act_ex", _ptr(x), M, K, a, _ptr(cm), _ptr(q), _ptr(s),
+              _stream(x.device))
+    return q, s
 
 
-def quantize_act(x: torch.Tensor):
-    """Per-token int8 activations: x bf16 [M,K] -> (xq int8 [M,K], sx fp32 [M])."""
-    return _quantize("w8a8_quantize_act", x, "x")
+def col_absmax(v: torch.Tensor, *, act: str = "none", out=None, accumulate: bool = False):
+    """Per-column max |T(v)| of a bf16 [R,K] matrix -> fp32 [K]. With accumulate=True the
+    maxima are merged into `out` (several calibration batches)."""
+    a = _act(act)
+    if out is None and accumulate:
+        raise ValueError("accumulate needs out")
+    _check(v, torch.bfloat16, 2, "v")
+    R, K = v.shape
+    if out is None:
+        out = torch.empty((K,), dtype=torch.float32, device=v.device)
+    _check(out, torch.float32, 1, "out")
+    if out.shape[0] != K:
+        raise ValueError("out must be [K]")
+    with torch.cuda.device(v.device):
+        _call("w8a8_col_absmax", _ptr(v), R, K, a, _ptr(out), int(bool(accumulate)),
+              _stream(v.device))
+    return out
+
+
+def smooth_factors(x_amax: torch.Tensor, w_amax: torch.Tensor, alpha: float = 0.5):
+    """SmoothQuant factors (s, s_inv), fp32 [K]: s = x_amax^alpha / w_amax^(1-alpha)."""
+    _check(x_amax, torch.float32, 1, "x_amax")
+    _check(w_amax, torch.float32, 1, "w_amax")
+    _same_device(x_amax, w_amax)
+    if x_amax.shape != w_amax.shape:
+        raise ValueError("x_amax and w_amax must both be [K]")
+    K = x_amax.shape[0]
+    s = torch.empty_like(x_amax)
+    si = torch.empty_like(x_amax)
+    with torch.cuda.device(x_amax.device):
+        _call("w8a8_smooth_factors", _ptr(x_amax), _ptr(w_amax), K, float(alpha), _ptr(s),
+              _ptr(si), _stream(x_amax.device))
+    return s, si
 
 
 def _workspace(nbytes: int, device, workspace):
@@ -196,9 +272,11 @@ def gemm(xq, x_scale, wq, w_scale, bias=None, *, tile: int = -1, out=None,
     return y
 
 
-def linear(x, wq, w_scale, bias=None, *, out=None, workspace=None):
+def linear(x, wq, w_scale, bias=None, *, act: str = "none", col_mul=None, out=None,
+           workspace=None):
     """The whole W8A8 linear: x bf16 [..., K] -> y bf16 [..., N] (per-token
-    quantization of x, int8 GEMM, fused dequantization + bias)."""
+    quantization of T(x) * col_mul, int8 GEMM, fused dequantization + bias)."""
+    a = _act(act)
     if not isinstance(x, torch.Tensor) or x.dtype != torch.bfloat16:
         raise TypeError("x must be a bf16 torch.Tensor")
     lead = x.shape[:-1]
@@ -214,14 +292,15 @@ def linear(x, wq, w_scale, bias=None, *, out=None, workspace=None):
     N = wq.shape[0]
     if wq.shape[1] != K or w_scale.shape[0] != N or (bias is not None and bias.shape[0] != N):
         raise ValueError("shape mismatch")
+    cm = _col_mul(col_mul, K, x.device)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
                                                 device=x.device)
     if M == 0 or N == 0:
         return y.reshape(*lead, N)
     ws = _workspace(linear_workspace_bytes(M, N, K), x.device, workspace)
     with torch.cuda.device(x.device):
-        _call("w8a8_linear", _ptr(x2), _ptr(wq), _ptr(w_scale), _ptr(bias), _ptr(y), M, N, K,
-              _ptr(ws), ws.numel() * ws.element_size(), _stream(x.device))
+        _call("w8a8_linear_ex", _ptr(x2), a, _ptr(cm), _ptr(wq), _ptr(w_scale), _ptr(bias),
+              _ptr(y), M, N, K, _ptr(ws), ws.numel() * ws.element_size(), _stream(x.device))
     return y.reshape(*lead, N)
 
 

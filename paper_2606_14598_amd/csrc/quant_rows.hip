@@ -6,6 +6,13 @@
 //   a = max_k |v[k]|, s = a / 127, q[k] = clamp(rne(v[k] * (127 / a)), -127, 127),
 // and a row with a == 0 or with 127/a overflowing float32 gets s = 0, q = 0.
 //
+// The rule can run on transformed values v[k] = T(x[k]) * c[k] instead of the bf16
+// inputs themselves: T is the identity or the exact GELU x * Phi(x) (the activation in
+// front of the MLP down-projection, applied here so that it costs no pass of its own),
+// and c is a per-input-channel multiplier, the run-time half of SmoothQuant (the recipe
+// of Section 3 smooths the activations by 1/s[k] and folds s[k] into the weights).
+// Both are evaluated in float32; the row maximum is then taken on float32 values.
+//
 // The kernel is HBM-bound (3 bytes moved per element: 2 read, 1 written). Rows whose
 // K fits the register file are read once with 16-byte loads, kept in VGPRs for the
 // second (quantizing) pass and written with 8-byte stores, by a persistent grid that
@@ -69,8 +76,7 @@ struct RowScale {
     float scale;  // a / 127, or 0 for a zero row
 };
 
-__device__ __forceinline__ RowScale row_scale(uint32_t amax_bits) {
-    float a = bf16_to_f32(amax_bits);
+__device__ __forceinline__ RowScale row_scale_f(float a) {
     float inv = 127.0f / a;     // correctly rounded (no fast-math)
     float s = a / 127.0f;
     bool zero = !(a > 0.0f) || !__builtin_isfinite(inv);
@@ -80,22 +86,73 @@ __device__ __forceinline__ RowScale row_scale(uint32_t amax_bits) {
     return r;
 }
 
+__device__ __forceinline__ RowScale row_scale(uint32_t amax_bits) {
+    return row_scale_f(bf16_to_f32(amax_bits));
+}
+
+// GELU(x) = x * Phi(x), Phi(x) = erfc(-x / sqrt(2)) / 2. The erfc form keeps the left
+// tail (x << 0, where 1 + erf(x / sqrt(2)) would cancel) to a few units in the last
+// place.
+__device__ __forceinline__ float gelu_f32(float x) {
+    return 0.5f * x * erfcf(x * -0.70710678118654752440f);
+}
+
+// The value the row rule sees: T(x), times the channel multiplier c when there is one.
+template <int ACT, bool CM>
+__device__ __forceinline__ float transform(float x, float c) {
+    float t = x;
+    if constexpr (ACT == ACT_GELU)
+        t = gelu_f32(x);
+    if constexpr (CM)
+        t = t * c;
+    return t;
+}
+
+// Code of a float32 value (transformed rows).
+__device__ __forceinline__ uint32_t code_f(float v, float inv) {
+    float r = __builtin_rintf(v * inv);
+    r = fminf(fmaxf(r, -127.0f), 127.0f);
+    return (uint32_t)((int)r) & 0xFFu;
+}
+
+__device__ __forceinline__ uint32_t abs_bits(float v) {
+    return __float_as_uint(v) & 0x7FFFFFFFu;
+}
+
 // Register-resident path, persistent and software-pipelined: TPR threads per row
 // (64 = one wavefront, 256 = the block), NV 16-byte vectors per thread (K % 8 == 0,
 // v 16-byte and q 8-byte aligned). Row group j of a block holds rows j*RPB .. j*RPB +
 // RPB - 1; block b handles row groups b, b + G, b + 2G, ... (G = gridDim.x) and loads
 // group j + G while it reduces, quantizes and stores group j, so the HBM reads of the
 // next rows overlap the work and the stores of the current ones.
-template <int TPR, int NV>
+// With a transform (ACT != ACT_NONE or a multiplier), each thread's columns are the
+// same for every row, so its multipliers are loaded once into registers; the
+// transformed row is held as float32 between the maximum and the coding pass.
+template <int TPR, int NV, int ACT, bool CM>
 __global__ void __launch_bounds__(256)
 quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
-               int8_t *__restrict__ q, float *__restrict__ scale) {
+               const float *__restrict__ colmul, int8_t *__restrict__ q,
+               float *__restrict__ scale) {
+    constexpr bool PLAIN = ACT == ACT_NONE && !CM;
     constexpr int RPB = 256 / TPR;
     const int t = threadIdx.x % TPR;
     const int sub = threadIdx.x / TPR;
     const int64_t nvec = K >> 3;
     const int64_t groups = (rows + RPB - 1) / RPB;
     __shared__ uint32_t part[RPB][TPR / 64];
+
+    float cmr[CM ? NV : 1][8];
+    if constexpr (CM) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int64_t vi = (int64_t)j * TPR + t;
+            const float4 *c4 = reinterpret_cast<const float4 *>(colmul) + 2 * vi;
+            const float4 lo = vi < nvec ? c4[0] : make_float4(0, 0, 0, 0);
+            const float4 hi = vi < nvec ? c4[1] : make_float4(0, 0, 0, 0);
+            cmr[j][0] = lo.x; cmr[j][1] = lo.y; cmr[j][2] = lo.z; cmr[j][3] = lo.w;
+            cmr[j][4] = hi.x; cmr[j][5] = hi.y; cmr[j][6] = hi.z; cmr[j][7] = hi.w;
+        }
+    }
 
     auto load = [&](uint4 (&d)[NV], int64_t grp) {
         const int64_t row = grp * RPB + sub;
@@ -113,9 +170,23 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
     auto process = [&](const uint4 (&d)[NV], int64_t grp) {
         const int64_t row = grp * RPB + sub;
         uint32_t m = 0;
+        float f[PLAIN ? 1 : NV][8];
+        if constexpr (PLAIN) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j)
-            m = max(m, absmax8(d[j]));
+            for (int j = 0; j < NV; ++j)
+                m = max(m, absmax8(d[j]));
+        } else {
+#pragma unroll
+            for (int j = 0; j < NV; ++j) {
+                const uint32_t w[4] = {d[j].x, d[j].y, d[j].z, d[j].w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t h = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
+                    f[j][e] = transform<ACT, CM>(bf16_to_f32(h), CM ? cmr[j][e] : 1.0f);
+                    m = max(m, abs_bits(f[j][e]));
+                }
+            }
+        }
         m = wave_max(m);
         if constexpr (TPR == 256) {
             if ((threadIdx.x & 63) == 0)
@@ -124,7 +195,7 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
             m = max(max(part[sub][0], part[sub][1]), max(part[sub][2], part[sub][3]));
             __syncthreads();   // part is rewritten by the next row group
         }
-        const RowScale rs = row_scale(m);
+        const RowScale rs = PLAIN ? row_scale(m) : row_scale_f(__uint_as_float(m));
         if (row >= rows)
             return;
         if (t == 0)
@@ -133,8 +204,20 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             const int64_t vi = (int64_t)j * TPR + t;
-            if (vi < nvec)
-                dst[vi] = code8(d[j], rs.inv);
+            if (vi < nvec) {
+                if constexpr (PLAIN) {
+                    dst[vi] = code8(d[j], rs.inv);
+                } else {
+                    uint32_t c[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        c[e] = code_f(f[j][e], rs.inv);
+                    uint2 o;
+                    o.x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+                    o.y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
+                    dst[vi] = o;
+                }
+            }
         }
     };
 
@@ -153,23 +236,32 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
 
 // General path: one 256-thread block per row, two passes over the row (the second
 // re-reads it, normally from L2). VEC selects 16-byte loads (K % 8 == 0 and aligned
-// pointers); otherwise every element is loaded and stored on its own, for any K and
-// any alignment.
-template <bool VEC>
+// pointers, plain rule only); otherwise every element is loaded and stored on its own,
+// for any K and any alignment, and a transform is evaluated in both passes.
+template <bool VEC, int ACT, bool CM>
 __global__ void __launch_bounds__(256)
 quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
-                int8_t *__restrict__ q, float *__restrict__ scale) {
+                const float *__restrict__ colmul, int8_t *__restrict__ q,
+                float *__restrict__ scale) {
+    constexpr bool PLAIN = ACT == ACT_NONE && !CM;
+    static_assert(PLAIN || !VEC, "transformed rows take the element path");
     const int64_t row = blockIdx.x;
     const int t = threadIdx.x;
     const uint16_t *src = v + row * K;
+    auto value = [&](int64_t k) {
+        return transform<ACT, CM>(bf16_to_f32(src[k]), CM ? colmul[k] : 1.0f);
+    };
     uint32_t m = 0;
     if constexpr (VEC) {
         const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
         for (int64_t vi = t; vi < (K >> 3); vi += 256)
             m = max(m, absmax8(s4[vi]));
-    } else {
+    } else if constexpr (PLAIN) {
         for (int64_t k = t; k < K; k += 256)
             m = max(m, (uint32_t)src[k] & 0x7FFFu);
+    } else {
+        for (int64_t k = t; k < K; k += 256)
+            m = max(m, abs_bits(value(k)));
     }
     m = wave_max(m);
     __shared__ uint32_t part[4];
@@ -177,7 +269,7 @@ quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
         part[t >> 6] = m;
     __syncthreads();
     m = max(max(part[0], part[1]), max(part[2], part[3]));
-    const RowScale rs = row_scale(m);
+    const RowScale rs = PLAIN ? row_scale(m) : row_scale_f(__uint_as_float(m));
     if (t == 0)
         scale[row] = rs.scale;
     int8_t *dst = q + row * K;
@@ -186,54 +278,144 @@ quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
         uint2 *d2 = reinterpret_cast<uint2 *>(dst);
         for (int64_t vi = t; vi < (K >> 3); vi += 256)
             d2[vi] = code8(s4[vi], rs.inv);
-    } else {
+    } else if constexpr (PLAIN) {
         for (int64_t k = t; k < K; k += 256)
             dst[k] = (int8_t)code((uint32_t)src[k], rs.inv);
+    } else {
+        for (int64_t k = t; k < K; k += 256)
+            dst[k] = (int8_t)code_f(value(k), rs.inv);
     }
 }
 
-template <int TPR, int NV>
-hipError_t launch_reg(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
-                      float *scale, hipStream_t s) {
+template <int TPR, int NV, int ACT, bool CM>
+hipError_t launch_reg(const uint16_t *v, int64_t rows, int64_t K, const float *colmul,
+                      int8_t *q, float *scale, hipStream_t s) {
     constexpr int RPB = 256 / TPR;
     const int64_t groups = (rows + RPB - 1) / RPB;
     // Persistent grid: a few blocks per CU, each walking row groups with prefetch.
     const int64_t max_blocks = 256 * 8;
     const int64_t blocks = groups < max_blocks ? groups : max_blocks;
-    hipLaunchKernelGGL((quant_rows_reg<TPR, NV>), dim3((unsigned)blocks), dim3(256), 0, s,
-                       v, rows, K, q, scale);
+    hipLaunchKernelGGL((quant_rows_reg<TPR, NV, ACT, CM>), dim3((unsigned)blocks), dim3(256),
+                       0, s, v, rows, K, colmul, q, scale);
     return hipGetLastError();
+}
+
+template <int ACT, bool CM>
+hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *colmul,
+                       int8_t *q, float *scale, hipStream_t s) {
+    constexpr bool PLAIN = ACT == ACT_NONE && !CM;
+    const bool vec = (K % 8 == 0) && (reinterpret_cast<uintptr_t>(v) % 16 == 0) &&
+                     (reinterpret_cast<uintptr_t>(q) % 8 == 0) &&
+                     (reinterpret_cast<uintptr_t>(colmul) % 16 == 0);
+    const int64_t nvec = K / 8;
+    if (vec && K > 0) {
+        if (nvec <= 64)
+            return launch_reg<64, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 128)
+            return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 256)
+            return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 512)
+            return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 1024)
+            return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 2048)
+            return launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+    }
+    if (PLAIN && vec)
+        hipLaunchKernelGGL((quant_rows_loop<PLAIN, ACT, CM>), dim3((unsigned)rows), dim3(256),
+                           0, s, v, rows, K, colmul, q, scale);
+    else
+        hipLaunchKernelGGL((quant_rows_loop<false, ACT, CM>), dim3((unsigned)rows), dim3(256),
+                           0, s, v, rows, K, colmul, q, scale);
+    return hipGetLastError();
+}
+
+// Calibration: per-column max |T(x)| over a block of rows, merged across blocks with
+// an unsigned atomic maximum on the float32 bit patterns (monotone for values >= 0).
+template <int ACT>
+__global__ void __launch_bounds__(256)
+col_absmax_kernel(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
+                  int64_t rows_per_block, uint32_t *__restrict__ amax) {
+    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k >= K)
+        return;
+    const int64_t r0 = (int64_t)blockIdx.y * rows_per_block;
+    const int64_t r1 = r0 + rows_per_block < rows ? r0 + rows_per_block : rows;
+    uint32_t m = 0;
+    for (int64_t r = r0; r < r1; ++r)
+        m = max(m, abs_bits(transform<ACT, false>(bf16_to_f32(v[r * K + k]), 1.0f)));
+    atomicMax(amax + k, m);
+}
+
+__global__ void __launch_bounds__(256) fill_zero_u32(uint32_t *p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n)
+        p[i] = 0u;
+}
+
+// SmoothQuant factors: s = ax^alpha / aw^(1 - alpha) (alpha = 1/2: sqrtf / sqrtf, each
+// correctly rounded); channels without a positive, finite pair, or whose factor is 0
+// or infinite, stay unsmoothed (s = 1). s_inv = 1 / s is the activation multiplier.
+__global__ void __launch_bounds__(256)
+smooth_factors_kernel(const float *__restrict__ ax, const float *__restrict__ aw, int64_t K,
+                      float alpha, float *__restrict__ s, float *__restrict__ s_inv) {
+    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k >= K)
+        return;
+    const float a = ax[k], b = aw[k];
+    float f = 1.0f;
+    if (a > 0.0f && b > 0.0f && __builtin_isfinite(a) && __builtin_isfinite(b)) {
+        f = alpha == 0.5f ? sqrtf(a) / sqrtf(b) : powf(a, alpha) / powf(b, 1.0f - alpha);
+        if (!(f > 0.0f) || !__builtin_isfinite(f))
+            f = 1.0f;
+    }
+    s[k] = f;
+    s_inv[k] = 1.0f / f;
 }
 
 }  // namespace
 
-hipError_t launch_quant_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
-                             float *scale, hipStream_t s) {
+hipError_t launch_quant_rows(const uint16_t *v, int64_t rows, int64_t K, int act,
+                             const float *colmul, int8_t *q, float *scale, hipStream_t s) {
     if (rows <= 0)
         return hipSuccess;
-    const bool vec = (K % 8 == 0) && (reinterpret_cast<uintptr_t>(v) % 16 == 0) &&
-                     (reinterpret_cast<uintptr_t>(q) % 8 == 0);
-    const int64_t nvec = K / 8;
-    if (vec && K > 0) {
-        if (nvec <= 64)
-            return launch_reg<64, 1>(v, rows, K, q, scale, s);
-        if (nvec <= 128)
-            return launch_reg<64, 2>(v, rows, K, q, scale, s);
-        if (nvec <= 256)
-            return launch_reg<64, 4>(v, rows, K, q, scale, s);
-        if (nvec <= 512)
-            return launch_reg<64, 8>(v, rows, K, q, scale, s);
-        if (nvec <= 1024)
-            return launch_reg<256, 4>(v, rows, K, q, scale, s);
-        if (nvec <= 2048)
-            return launch_reg<256, 8>(v, rows, K, q, scale, s);
+    if (act == ACT_GELU)
+        return colmul ? launch_rows<ACT_GELU, true>(v, rows, K, colmul, q, scale, s)
+                      : launch_rows<ACT_GELU, false>(v, rows, K, colmul, q, scale, s);
+    return colmul ? launch_rows<ACT_NONE, true>(v, rows, K, colmul, q, scale, s)
+                  : launch_rows<ACT_NONE, false>(v, rows, K, colmul, q, scale, s);
+}
+
+hipError_t launch_col_absmax(const uint16_t *v, int64_t rows, int64_t K, int act,
+                             float *amax, bool accumulate, hipStream_t s) {
+    if (K <= 0)
+        return hipSuccess;
+    uint32_t *bits = reinterpret_cast<uint32_t *>(amax);
+    const unsigned kb = (unsigned)((K + 255) / 256);
+    if (!accumulate)
+        hipLaunchKernelGGL(fill_zero_u32, dim3(kb), dim3(256), 0, s, bits, K);
+    if (rows > 0) {
+        int64_t rpb = 32;
+        while ((rows + rpb - 1) / rpb > 65535)
+            rpb *= 2;
+        const dim3 grid(kb, (unsigned)((rows + rpb - 1) / rpb));
+        if (act == ACT_GELU)
+            hipLaunchKernelGGL(col_absmax_kernel<ACT_GELU>, grid, dim3(256), 0, s, v, rows, K,
+                               rpb, bits);
+        else
+            hipLaunchKernelGGL(col_absmax_kernel<ACT_NONE>, grid, dim3(256), 0, s, v, rows, K,
+                               rpb, bits);
     }
-    if (vec)
-        hipLaunchKernelGGL((quant_rows_loop<true>), dim3((unsigned)rows), dim3(256), 0, s,
-                           v, rows, K, q, scale);
-    else
-        hipLaunchKernelGGL((quant_rows_loop<false>), dim3((unsigned)rows), dim3(256), 0, s,
-                           v, rows, K, q, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_smooth_factors(const float *ax, const float *aw, int64_t K, float alpha,
+                                 float *smooth, float *smooth_inv, hipStream_t s) {
+    if (K <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(smooth_factors_kernel, dim3((unsigned)((K + 255) / 256)), dim3(256), 0,
+                       s, ax, aw, K, alpha, smooth, smooth_inv);
     return hipGetLastError();
 }
 

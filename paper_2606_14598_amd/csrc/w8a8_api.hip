@@ -20,6 +20,10 @@ w8a8_status from_hip(hipError_t e) { return e == hipSuccess ? W8A8_OK : W8A8_ERR
 
 bool aligned16(const void *p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
 
+static_assert(W8A8_ACT_NONE == ACT_NONE && W8A8_ACT_GELU == ACT_GELU, "act codes");
+
+bool act_ok(int act) { return act == W8A8_ACT_NONE || act == W8A8_ACT_GELU; }
+
 w8a8_status check_quant(const void *v, int64_t rows, int64_t K, const void *q,
                         const void *scale) {
     if (rows < 0 || K < 0 || !product_ok(rows, K))
@@ -78,20 +82,59 @@ w8a8_status run_gemm(const int8_t *xq, const float *sx, const int8_t *wq, const 
 #pragma GCC visibility push(default)
 extern "C" {
 
-w8a8_status w8a8_quantize_weight(const uint16_t *w, int64_t N, int64_t K, int8_t *wq,
-                                 float *w_scale, void *stream) {
+w8a8_status w8a8_quantize_weight_ex(const uint16_t *w, int64_t N, int64_t K,
+                                    const float *col_mul, int8_t *wq, float *w_scale,
+                                    void *stream) {
     const w8a8_status st = check_quant(w, N, K, wq, w_scale);
     if (st != W8A8_OK)
         return st;
-    return from_hip(launch_quant_rows(w, N, K, wq, w_scale, as_stream(stream)));
+    return from_hip(launch_quant_rows(w, N, K, ACT_NONE, col_mul, wq, w_scale,
+                                      as_stream(stream)));
+}
+
+w8a8_status w8a8_quantize_weight(const uint16_t *w, int64_t N, int64_t K, int8_t *wq,
+                                 float *w_scale, void *stream) {
+    return w8a8_quantize_weight_ex(w, N, K, nullptr, wq, w_scale, stream);
+}
+
+w8a8_status w8a8_quantize_act_ex(const uint16_t *x, int64_t M, int64_t K, int act,
+                                 const float *col_mul, int8_t *xq, float *x_scale,
+                                 void *stream) {
+    if (!act_ok(act))
+        return W8A8_ERR_ARG;
+    const w8a8_status st = check_quant(x, M, K, xq, x_scale);
+    if (st != W8A8_OK)
+        return st;
+    return from_hip(launch_quant_rows(x, M, K, act, col_mul, xq, x_scale, as_stream(stream)));
 }
 
 w8a8_status w8a8_quantize_act(const uint16_t *x, int64_t M, int64_t K, int8_t *xq,
                               float *x_scale, void *stream) {
-    const w8a8_status st = check_quant(x, M, K, xq, x_scale);
-    if (st != W8A8_OK)
-        return st;
-    return from_hip(launch_quant_rows(x, M, K, xq, x_scale, as_stream(stream)));
+    return w8a8_quantize_act_ex(x, M, K, W8A8_ACT_NONE, nullptr, xq, x_scale, stream);
+}
+
+w8a8_status w8a8_col_absmax(const uint16_t *v, int64_t R, int64_t K, int act, float *amax,
+                            int accumulate, void *stream) {
+    if (!act_ok(act))
+        return W8A8_ERR_ARG;
+    if (R < 0 || K < 0 || !product_ok(R, K))
+        return W8A8_ERR_SHAPE;
+    if (K > 0 && (!amax || (R > 0 && !v)))
+        return W8A8_ERR_NULL;
+    return from_hip(launch_col_absmax(v, R, K, act, amax, accumulate != 0, as_stream(stream)));
+}
+
+w8a8_status w8a8_smooth_factors(const float *x_amax, const float *w_amax, int64_t K,
+                                float alpha, float *smooth, float *smooth_inv,
+                                void *stream) {
+    if (!(alpha >= 0.0f && alpha <= 1.0f))
+        return W8A8_ERR_ARG;
+    if (K < 0)
+        return W8A8_ERR_SHAPE;
+    if (K > 0 && (!x_amax || !w_amax || !smooth || !smooth_inv))
+        return W8A8_ERR_NULL;
+    return from_hip(launch_smooth_factors(x_amax, w_amax, K, alpha, smooth, smooth_inv,
+                                          as_stream(stream)));
 }
 
 size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
@@ -128,10 +171,12 @@ size_t w8a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
            w8a8_gemm_workspace_bytes(M, N, K);
 }
 
-w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scale,
-                        const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
-                        int64_t K, void *workspace, size_t workspace_bytes,
-                        void *stream) {
+w8a8_status w8a8_linear_ex(const uint16_t *x, int act, const float *col_mul,
+                           const int8_t *wq, const float *w_scale, const uint16_t *bias,
+                           uint16_t *y, int64_t M, int64_t N, int64_t K, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    if (!act_ok(act))
+        return W8A8_ERR_ARG;
     if (M < 0 || N < 0 || K < 0 || !product_ok(M, K) || !product_ok(N, K) ||
         !product_ok(M, N))
         return W8A8_ERR_SHAPE;
@@ -151,11 +196,19 @@ w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scal
                                           align_up((size_t)(M * K)));
     char *gws = reinterpret_cast<char *>(sx) + align_up((size_t)M * sizeof(float));
     hipStream_t s = as_stream(stream);
-    hipError_t e = launch_quant_rows(x, M, K, xq, sx, s);
+    hipError_t e = launch_quant_rows(x, M, K, act, col_mul, xq, sx, s);
     if (e != hipSuccess)
         return W8A8_ERR_HIP;
     return run_gemm(xq, sx, wq, w_scale, bias, y, EPI_BF16, M, N, K, gws,
                     workspace_bytes - (size_t)(gws - static_cast<char *>(workspace)), -1, s);
+}
+
+w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scale,
+                        const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                        int64_t K, void *workspace, size_t workspace_bytes,
+                        void *stream) {
+    return w8a8_linear_ex(x, W8A8_ACT_NONE, nullptr, wq, w_scale, bias, y, M, N, K,
+                          workspace, workspace_bytes, stream);
 }
 
 w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *acc,

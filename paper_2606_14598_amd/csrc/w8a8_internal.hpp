@@ -8,10 +8,21 @@
 namespace w8a8 {
 
 // ---------------------------------------------------------------- quantizer
-// Launches the per-row absmax quantizer over a [rows, K] bf16 matrix on `stream`.
+enum Act : int { ACT_NONE = 0, ACT_GELU = 1 };
+
+// Launches the per-row absmax quantizer over a [rows, K] bf16 matrix on `stream`, on
+// the values T(x) * colmul[k] (T = identity or GELU; colmul [K] float32 or nullptr).
 // Returns hipSuccess or the launch error.
-hipError_t launch_quant_rows(const uint16_t *v, int64_t rows, int64_t K, int8_t *q,
-                             float *scale, hipStream_t stream);
+hipError_t launch_quant_rows(const uint16_t *v, int64_t rows, int64_t K, int act,
+                             const float *colmul, int8_t *q, float *scale,
+                             hipStream_t stream);
+// Per-column max |T(x)| of a [rows, K] bf16 matrix into amax [K] (merged with its
+// current contents when `accumulate`, else replacing them).
+hipError_t launch_col_absmax(const uint16_t *v, int64_t rows, int64_t K, int act,
+                             float *amax, bool accumulate, hipStream_t stream);
+// SmoothQuant factors and their reciprocals from per-channel maxima of X and W.
+hipError_t launch_smooth_factors(const float *ax, const float *aw, int64_t K, float alpha,
+                                 float *smooth, float *smooth_inv, hipStream_t stream);
 
 // ---------------------------------------------------------------- GEMM
 enum Epilogue : int { EPI_BF16 = 0, EPI_I32 = 1 };

@@ -12,7 +12,11 @@ round-to-nearest-even by torch's dtype conversion):
     17 and 3K/4 + 5 (the activation-outlier pattern SmoothQuant-style W8A8 recipes are
     built for, Section 2 "W8A8 PTQ recipe and outliers").
   * "gelu" X: exact-erf GELU of N(0, 1), no outlier channels (the input of an MLP
-    down-projection).
+    down-projection). The GELU here (scipy's erf) only shapes the distribution;
+    neither the oracle nor the HIP path uses it.
+  * "preact" X: N(0, 1), no outlier channels: the pre-activation of that MLP, drawn
+    from the same numbers as "gelu" (same seed, same draw), for the path that applies
+    GELU inside the quantizer.
   * "student_t" X: Student-t with 3 degrees of freedom, no outlier channels
     (heavy-tailed activations).
   * W ~ N(0, 0.02) times a per-output-channel multiplier drawn from U(0.5, 2).
@@ -41,7 +45,7 @@ class Shape:
     M: int
     K: int
     N: int
-    dist: str = "outlier"      # "outlier" | "gelu" | "student_t"
+    dist: str = "outlier"      # "outlier" | "gelu" | "preact" | "student_t"
     seed: int = 0
 
     @property
@@ -110,6 +114,8 @@ def draw_x(rng: np.random.Generator, M: int, K: int, dist: str) -> np.ndarray:
                 x[:, c] *= np.float32(20.0)
     elif dist == "gelu":
         x = _erf_gelu(rng.standard_normal((M, K), dtype=np.float32))
+    elif dist == "preact":
+        x = rng.standard_normal((M, K), dtype=np.float32)
     elif dist == "student_t":
         x = rng.standard_t(3, size=(M, K)).astype(np.float32)
     else:

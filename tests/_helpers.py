@@ -40,3 +40,28 @@ def assert_bf16_parity(got_bits, want_bits, what=""):
     assert d.max() <= 1, f"{what}: max ulp {d.max()} at {np.unravel_index(d.argmax(), d.shape)}"
     assert cos >= 0.99999, f"{what}: cosine {cos}"
     return stats
+
+
+# Device round trips for the GPU tests (torch is imported lazily: the CPU suite does
+# not need it here).
+def dev_bf16(bits):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def dev_f32(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def host_bits(t):
+    import torch
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+def say(*a):
+    print(*a, flush=True)

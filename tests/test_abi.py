@@ -122,3 +122,40 @@ def test_python_binding_rejects_cpu_tensors():
         w8a8.quantize_act(x)
     with pytest.raises(TypeError):
         w8a8.quantize_act(x.float())
+
+
+def test_transform_and_smoothing_validation(lib):
+    P = ctypes.c_void_p
+    fake = P(256)
+    # unknown activation transform
+    assert lib.w8a8_quantize_act_ex(fake, 4, 16, 2, None, fake, fake, None) == ERR_ARG
+    assert lib.w8a8_quantize_act_ex(fake, 4, 16, -1, None, fake, fake, None) == ERR_ARG
+    assert lib.w8a8_linear_ex(fake, 7, None, fake, fake, None, fake, 4, 8, 16, fake, 1 << 20,
+                              None) == ERR_ARG
+    assert lib.w8a8_col_absmax(fake, 4, 16, 3, fake, 0, None) == ERR_ARG
+    # shapes and pointers
+    assert lib.w8a8_quantize_act_ex(fake, -4, 16, 1, None, fake, fake, None) == ERR_SHAPE
+    assert lib.w8a8_quantize_weight_ex(fake, 4, 16, fake, None, fake, None) == ERR_NULL
+    assert lib.w8a8_col_absmax(fake, -1, 16, 0, fake, 0, None) == ERR_SHAPE
+    assert lib.w8a8_col_absmax(fake, 4, 16, 0, None, 0, None) == ERR_NULL
+    assert lib.w8a8_col_absmax(None, 4, 16, 0, fake, 0, None) == ERR_NULL
+    # alpha must lie in [0, 1]
+    for alpha in (-0.1, 1.5, float("nan")):
+        assert lib.w8a8_smooth_factors(fake, fake, 16, alpha, fake, fake, None) == ERR_ARG
+    assert lib.w8a8_smooth_factors(fake, None, 16, 0.5, fake, fake, None) == ERR_NULL
+    assert lib.w8a8_smooth_factors(fake, fake, -1, 0.5, fake, fake, None) == ERR_SHAPE
+    # empty problems are no-ops
+    assert lib.w8a8_smooth_factors(None, None, 0, 0.5, None, None, None) == OK
+    assert lib.w8a8_col_absmax(None, 0, 0, 1, None, 0, None) == OK
+    assert lib.w8a8_quantize_act_ex(None, 0, 16, 1, None, None, None, None) == OK
+    assert lib.w8a8_linear_ex(None, 1, None, None, None, None, None, 0, 8, 16, None, 0,
+                              None) == OK
+
+
+def test_python_binding_checks_transform_arguments():
+    import torch
+    x = torch.zeros(4, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        w8a8.quantize_act(x, act="relu")
+    with pytest.raises(ValueError):
+        w8a8.col_absmax(x, accumulate=True)
