@@ -18,6 +18,7 @@ Prints one JSON line. Besides the required fields it carries:
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
        python bench.py --all-shapes           (every workload shape, one JSON line each)
+       python bench.py --recipe               (GELU / SmoothQuant quantizer, shared X)
        python bench.py --copy-calibration     (a known-size copy for counter scaling)
 """
 from __future__ import annotations
@@ -413,6 +414,115 @@ def all_shapes(args):
             del xd, wd, bd, wq, sw, xq, sx, y, ws
 
 
+def recipe(args):
+    """The recipe's extra steps: GELU and the SmoothQuant multiplier inside the per-token
+    quantizer (against a separate GELU pass), the whole GELU down-projection, the
+    multiplier's cost in a linear, and one quantization shared by two linears. One JSON
+    line per measurement; times are HIP-graph replays of 20 calls."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    import paper_2606_14598_amd as w8a8
+    import synth_inputs as si
+    dev = torch.device("cuda:0")
+
+    def emit(rec):
+        print(json.dumps(rec), flush=True)
+
+    # 1. quantizer variants on activation matrices of the MLP shapes
+    for (M, K, tag) in [(2560, 4096, "attn_in"), (2560, 16384, "mlp_down_in"),
+                        (4608, 12288, "paper_ffn_down_in")]:
+        h, _, _ = si.make_inputs((M, K, 1), seed=20260 + K, dist="preact")
+        hd = dev_bf16(h, dev)
+        cm = torch.rand(K, device=dev) * 4 + 0.25
+        g = F.gelu(hd)
+        base = 3 * M * K + 4 * M
+        t = {
+            "plain": graph_ms(lambda: w8a8.quantize_act(hd)),
+            "colmul": graph_ms(lambda: w8a8.quantize_act(hd, col_mul=cm)),
+            "gelu": graph_ms(lambda: w8a8.quantize_act(hd, act="gelu")),
+            "gelu_colmul": graph_ms(lambda: w8a8.quantize_act(hd, act="gelu", col_mul=cm)),
+            "torch_gelu_then_plain": graph_ms(lambda: w8a8.quantize_act(F.gelu(hd))),
+            "torch_gelu_alone": graph_ms(lambda: F.gelu(hd)),
+        }
+        rec = {"what": "quantizer", "shape": tag, "M": M, "K": K,
+               "us": {k: round(v * 1e3, 2) for k, v in t.items()},
+               "GB_s": {k: round((base + (4 * K if "colmul" in k else 0)) / t[k] / 1e6, 1)
+                        for k in ("plain", "colmul", "gelu", "gelu_colmul")},
+               "gelu_fused_speedup_vs_separate_pass": round(t["torch_gelu_then_plain"] / t["gelu"], 3)}
+        emit(rec)
+        del hd, g, cm
+
+    # 2. the GELU down-projection as one call against GELU + linear and bf16
+    for (cfg, name) in [(2, "mlp_down"), (3, "mlp_down")]:
+        shp = si.workload(cfg, name)
+        M, N, K = shp.M, shp.N, shp.K
+        h, w, b = si.make_inputs(shp, dist="preact")
+        hd, wd, bd = dev_bf16(h, dev), dev_bf16(w, dev), dev_bf16(b, dev)
+        wq, sw = w8a8.quantize_weight(wd)
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+        fused = graph_ms(lambda: w8a8.linear(hd, wq, sw, bd, act="gelu", out=y, workspace=ws))
+        sep = graph_ms(lambda: w8a8.linear(F.gelu(hd), wq, sw, bd, out=y, workspace=ws))
+        bf = graph_ms(lambda: F.linear(F.gelu(hd), wd, bd))
+        emit({"what": "gelu_down_projection", "config": cfg, "M": M, "K": K, "N": N,
+              "us": {"w8a8_linear_gelu": round(fused * 1e3, 2),
+                     "torch_gelu_then_w8a8_linear": round(sep * 1e3, 2),
+                     "torch_gelu_then_bf16_linear": round(bf * 1e3, 2)},
+              "tops_fused": round(gemm_ops(M, N, K) / fused / 1e9, 1),
+              "speedup_vs_separate_gelu": round(sep / fused, 3),
+              "speedup_vs_bf16": round(bf / fused, 3)})
+        del hd, wd, bd, wq, sw, y, ws
+
+    # 3. a smoothed linear (multiplier in the quantizer) against the plain one
+    shp = si.workload(1, "attn_proj")
+    M, N, K = shp.M, shp.N, shp.K
+    x, w, b = si.make_inputs(shp)
+    xd, wd, bd = dev_bf16(x, dev), dev_bf16(w, dev), dev_bf16(b, dev)
+    ax = w8a8.col_absmax(xd)
+    aw = w8a8.col_absmax(wd)
+    sm, sm_inv = w8a8.smooth_factors(ax, aw, 0.5)
+    wq, sw = w8a8.quantize_weight(wd)
+    wqs, sws = w8a8.quantize_weight(wd, col_mul=sm)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+    plain = graph_ms(lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws))
+    smooth = graph_ms(lambda: w8a8.linear(xd, wqs, sws, bd, col_mul=sm_inv, out=y, workspace=ws))
+    calib = graph_ms(lambda: w8a8.col_absmax(xd, out=ax, accumulate=True))
+    emit({"what": "smoothquant_linear", "M": M, "K": K, "N": N,
+          "us": {"plain": round(plain * 1e3, 2), "smoothed": round(smooth * 1e3, 2),
+                 "calibration_col_absmax_per_batch": round(calib * 1e3, 2)},
+          "overhead_pct": round(100 * (smooth / plain - 1), 2)})
+    del xd, wd, bd, wq, sw, wqs, sws, y, ws
+
+    # 4. one quantization shared by two linears reading the same activations
+    x, _, _ = si.make_inputs((2560, 4096, 1), seed=20261)
+    xd = dev_bf16(x, dev)
+    lins = []
+    for N, seed in ((12288, 11), (16384, 12)):
+        _, w, b = si.make_inputs((1, 4096, N), seed=seed)
+        wq, sw = w8a8.quantize_weight(dev_bf16(w, dev))
+        lins.append((wq, sw, dev_bf16(b, dev), torch.empty((2560, N), dtype=torch.bfloat16,
+                                                           device=dev)))
+    ws = torch.empty(w8a8.linear_workspace_bytes(2560, 16384, 4096), dtype=torch.uint8,
+                     device=dev)
+    xq = torch.empty((2560, 4096), dtype=torch.int8, device=dev)
+
+    def two_linears():
+        for wq, sw, bd, y in lins:
+            w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws)
+
+    def shared():
+        q, s = w8a8.quantize_act(xd)
+        for wq, sw, bd, y in lins:
+            w8a8.gemm(q, s, wq, sw, bd, out=y)
+
+    t2, ts = graph_ms(two_linears), graph_ms(shared)
+    emit({"what": "shared_quantization", "M": 2560, "K": 4096, "N": [12288, 16384],
+          "us": {"two_linears": round(t2 * 1e3, 2), "quantize_once_two_gemms": round(ts * 1e3, 2)},
+          "saving_pct": round(100 * (1 - ts / t2), 2)})
+
+
 def copy_calibration():
     """A plain device copy of known size (for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)."""
     import torch
@@ -438,6 +548,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--all-shapes", action="store_true",
                     help="time every workload shape (one JSON line each)")
+    ap.add_argument("--recipe", action="store_true",
+                    help="time GELU / SmoothQuant in the quantizer and shared quantization")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -452,6 +564,9 @@ def main():
         return
     if args.all_shapes:
         all_shapes(args)
+        return
+    if args.recipe:
+        recipe(args)
         return
     rec = run(args)
     print(json.dumps(rec), flush=True)

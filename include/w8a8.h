@@ -130,10 +130,13 @@ w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *ac
  *
  * act selects a transform T applied to the bf16 input before the multiplier:
  *   W8A8_ACT_NONE  T(x) = x
- *   W8A8_ACT_GELU  T(x) = x * Phi(x), the exact (erf) GELU, evaluated in float32 to
- *                  within a few units in the last place of the exact value. It feeds
- *                  the MLP down-projection from the pre-activation, with no GELU pass
- *                  of its own.
+ *   W8A8_ACT_GELU  T(x) = x * Phi(x), the exact (erf) GELU, evaluated in float32
+ *                  through a Chebyshev fit of erfc (Numerical Recipes' erfcc,
+ *                  fractional error < 1.2e-7) on the hardware reciprocal and exp2:
+ *                  relative error about 3e-7 where |x| < 4, growing in the far left
+ *                  tail with the float32 rounding of x^2 / 2 (there GELU(x) is below
+ *                  1e-4 |x|). It feeds the MLP down-projection from the
+ *                  pre-activation, with no GELU pass of its own.
  * The quantizer then applies the row rule above to v[k] = T(x[k]) * col_mul[k]
  * (float32 multiply; col_mul NULL means no multiplier). Any other act value returns
  * W8A8_ERR_ARG. */
