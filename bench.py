@@ -19,6 +19,7 @@ Prints one JSON line. Besides the required fields it carries:
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
        python bench.py --all-shapes           (every workload shape, one JSON line each)
        python bench.py --recipe               (GELU / SmoothQuant quantizer, shared X)
+       python bench.py --paper-shapes         (the paper's five shapes, tuned vs untuned)
        python bench.py --copy-calibration     (a known-size copy for counter scaling)
 """
 from __future__ import annotations
@@ -351,6 +352,9 @@ def run(args) -> dict:
     return rec
 
 
+FIXED_TILE = 0   # one configuration for every shape: the untuned-by-design arm
+
+
 def graph_ms(fn, iters: int = 20) -> float:
     """Mean ms per call of fn, `iters` calls captured in one HIP graph and replayed (no
     host launch overhead in the measurement, which matters for microsecond shapes)."""
@@ -523,6 +527,70 @@ def recipe(args):
           "saving_pct": round(100 * (1 - ts / t2), 2)})
 
 
+def paper_shapes(args):
+    """The paper's five model shapes over its token counts (Section 3, "Target
+    architecture"; Section 5 and Table 1): the fused GEMM with the tuned table's tile,
+    with the fallback rule's tile and with one fixed tile (the tuning ablation of
+    Section 3, "Why autotuning is load-bearing"), the whole linear (per-token quantizer
+    + fused GEMM) and bf16 F.linear, on the same synthetic inputs. One JSON line per
+    (shape, M), then one per shape with the ranges over M."""
+    import torch
+    import torch.nn.functional as F
+    import paper_2606_14598_amd as w8a8
+    import synth_inputs as si
+    dev = torch.device("cuda:0")
+    for name, N, K in si.PAPER_SHAPES:
+        recs = []
+        for M in si.PAPER_M:
+            shp = si.paper_shape(name, M)
+            x, w, b = si.make_inputs(shp)
+            xd = dev_bf16(x, dev)
+            del x
+            wd, bd = dev_bf16(w, dev), dev_bf16(b, dev)
+            wq, sw = w8a8.quantize_weight(wd)
+            xq, sx = w8a8.quantize_act(xd)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8,
+                             device=dev)
+            ops = gemm_ops(M, N, K)
+            it = 20 if ops < 5e14 else 5
+            ids = {"tuned": w8a8.select_tile(M, N, K), "default": w8a8.default_tile(M, N, K),
+                   "fixed": FIXED_TILE}
+            t = {}
+            for arm, tid in ids.items():
+                same = [a for a in t if ids[a] == tid]
+                t[arm] = t[same[0]] if same else graph_ms(
+                    lambda: w8a8.gemm(xq, sx, wq, sw, bd, tile=tid, out=y), it)
+            t["linear"] = graph_ms(lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws), it)
+            t["bf16"] = graph_ms(lambda: F.linear(xd, wd, bd), it)
+            rec = {"what": "paper_shape", "shape": name, "M": M, "N": N, "K": K,
+                   "tiles": {a: w8a8.tile_name(i) for a, i in ids.items()},
+                   "us": {a: round(v * 1e3, 2) for a, v in t.items()},
+                   "tops": {a: round(ops / t[a] / 1e9, 1) for a in ("tuned", "linear", "bf16")},
+                   "gemm_pct_int8_peak": round(100 * ops / t["tuned"] / 1e9 / PEAK_INT8_TOPS, 2),
+                   "speedup_vs_bf16": {"gemm_tuned": round(t["bf16"] / t["tuned"], 3),
+                                       "gemm_default": round(t["bf16"] / t["default"], 3),
+                                       "gemm_fixed": round(t["bf16"] / t["fixed"], 3),
+                                       "linear": round(t["bf16"] / t["linear"], 3)},
+                   "tuned_over_default": round(t["default"] / t["tuned"], 3),
+                   "tuned_over_fixed": round(t["fixed"] / t["tuned"], 3)}
+            print(json.dumps(rec), flush=True)
+            recs.append(rec)
+            del xd, wd, bd, wq, sw, xq, sx, y, ws
+            torch.cuda.empty_cache()
+
+        def rng(key, sub):
+            v = [r[key][sub] for r in recs]
+            return [min(v), max(v)]
+        print(json.dumps({"what": "paper_shape_summary", "shape": name, "N": N, "K": K,
+                          "M": si.PAPER_M,
+                          "gemm_vs_bf16": rng("speedup_vs_bf16", "gemm_tuned"),
+                          "gemm_default_vs_bf16": rng("speedup_vs_bf16", "gemm_default"),
+                          "gemm_fixed_vs_bf16": rng("speedup_vs_bf16", "gemm_fixed"),
+                          "linear_vs_bf16": rng("speedup_vs_bf16", "linear"),
+                          "tuned_tops": rng("tops", "tuned")}), flush=True)
+
+
 def copy_calibration():
     """A plain device copy of known size (for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)."""
     import torch
@@ -548,6 +616,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--all-shapes", action="store_true",
                     help="time every workload shape (one JSON line each)")
+    ap.add_argument("--paper-shapes", action="store_true",
+                    help="the paper's five model shapes over M = 512..16384, tuned vs untuned")
     ap.add_argument("--recipe", action="store_true",
                     help="time GELU / SmoothQuant in the quantizer and shared quantization")
     args = ap.parse_args()
@@ -567,6 +637,9 @@ def main():
         return
     if args.recipe:
         recipe(args)
+        return
+    if args.paper_shapes:
+        paper_shapes(args)
         return
     rec = run(args)
     print(json.dumps(rec), flush=True)

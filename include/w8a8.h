@@ -103,11 +103,15 @@ w8a8_status w8a8_gemm_acc_i32(const int8_t *xq, const int8_t *wq, int32_t *acc,
 
 /* Tile configurations (the per-shape table chosen offline, Section 3, "Why
  * autotuning is load-bearing"). w8a8_select_tile returns the id the table picks for a
- * shape; the _ex variants run a given id (-1 = the table's choice) for offline sweeps
- * and tests. An id outside [0, w8a8_tile_count()) returns W8A8_ERR_ARG. */
+ * shape (M within an entry's token range, N and K equal), else the fallback rule's;
+ * w8a8_default_tile returns the fallback rule's choice alone, the untuned arm of the
+ * tuning ablation. Both return -1 for M <= 0, N <= 0 or K < 0. The _ex variants run a
+ * given id (-1 = the table's choice) for offline sweeps and tests. An id outside
+ * [0, w8a8_tile_count()) returns W8A8_ERR_ARG. */
 int w8a8_tile_count(void);
 const char *w8a8_tile_name(int tile_id);
 int w8a8_select_tile(int64_t M, int64_t N, int64_t K);
+int w8a8_default_tile(int64_t M, int64_t N, int64_t K);
 
 w8a8_status w8a8_gemm_ex(const int8_t *xq, const float *x_scale, const int8_t *wq,
                          const float *w_scale, const uint16_t *bias, uint16_t *y,

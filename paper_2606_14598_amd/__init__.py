@@ -30,7 +30,7 @@ import torch
 
 __all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
            "col_absmax", "smooth_factors", "ACTS",
-           "tile_count", "tile_name", "select_tile", "gemm_workspace_bytes",
+           "tile_count", "tile_name", "select_tile", "default_tile", "gemm_workspace_bytes",
            "linear_workspace_bytes", "library_path", "load_library", "W8A8Error",
            "MAX_K", "version"]
 
@@ -80,6 +80,7 @@ def load_library():
         "w8a8_tile_count": ([], INT),
         "w8a8_tile_name": ([INT], ctypes.c_char_p),
         "w8a8_select_tile": ([I64, I64, I64], INT),
+        "w8a8_default_tile": ([I64, I64, I64], INT),
         "w8a8_status_string": ([INT], ctypes.c_char_p),
         "w8a8_version": ([], ctypes.c_char_p),
     }
@@ -142,6 +143,11 @@ def tile_name(tile_id: int) -> str:
 
 def select_tile(M: int, N: int, K: int) -> int:
     return int(load_library().w8a8_select_tile(M, N, K))
+
+
+def default_tile(M: int, N: int, K: int) -> int:
+    """The fallback rule's tile for a shape, ignoring the offline table."""
+    return int(load_library().w8a8_default_tile(M, N, K))
 
 
 def gemm_workspace_bytes(M: int, N: int, K: int) -> int:

@@ -844,10 +844,34 @@ struct TableEntry {
 };
 #include "tile_table.inc"
 
+static_assert(sizeof(kTileRate) / sizeof(kTileRate[0]) == kNumTiles, "one rate per tile");
+
+// Shapes without a table entry. Above 128 tokens a wave-quantization cost model picks
+// the tile: a launch of T workgroups on 256 CUs takes ceil(T / 256) rounds, each as long
+// as one tile's work (TM x TN x K) at the tile's sustained rate (kTileRate, measured
+// offline); K is common to every candidate and drops out. With few tokens the
+// weight-streaming kernels take over.
 int fallback_tile(int64_t M, int64_t N, int64_t K) {
     (void)K;
-    // Prefer the largest tile that still gives at least one workgroup per CU.
     const int64_t cus = 256;
+    if (M > 128) {
+        int best = -1;
+        double best_cost = 0.0;
+        for (int id = 0; id < kNumTiles; ++id) {
+            if (!(kTileRate[id] > 0.0f))
+                continue;
+            const TileInfo &t = kTiles[id].info;
+            const int64_t tiles = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
+            const int64_t rounds = (tiles + cus - 1) / cus;
+            const double cost = (double)rounds * t.tm * t.tn / kTileRate[id];
+            if (best < 0 || cost < best_cost) {
+                best = id;
+                best_cost = cost;
+            }
+        }
+        if (best >= 0)
+            return best;
+    }
     for (int id : {0, 2, 3, 4, 12}) {
         const TileInfo &t = kTiles[id].info;
         const int64_t tiles = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
@@ -873,6 +897,8 @@ int tile_count() { return kNumTiles; }
 const TileInfo *tile_info(int id) {
     return (id >= 0 && id < kNumTiles) ? &kTiles[id].info : nullptr;
 }
+
+int default_tile(int64_t M, int64_t N, int64_t K) { return fallback_tile(M, N, K); }
 
 int select_tile(int64_t M, int64_t N, int64_t K) {
     for (const TableEntry &e : kTileTable) {

@@ -246,6 +246,12 @@ int w8a8_select_tile(int64_t M, int64_t N, int64_t K) {
     return select_tile(M, N, K);
 }
 
+int w8a8_default_tile(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K < 0)
+        return -1;
+    return default_tile(M, N, K);
+}
+
 const char *w8a8_status_string(w8a8_status status) {
     switch (status) {
     case W8A8_OK: return "ok";

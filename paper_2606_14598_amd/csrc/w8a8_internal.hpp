@@ -48,6 +48,8 @@ int tile_count();
 const TileInfo *tile_info(int id);
 // Table lookup of the tile id for a shape (offline-chosen, with a fallback rule).
 int select_tile(int64_t M, int64_t N, int64_t K);
+// The fallback rule alone (what a shape gets without a table entry).
+int default_tile(int64_t M, int64_t N, int64_t K);
 // Extra device scratch a tile needs for a shape (0 for the data-parallel tiles).
 size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K);
 // Launch tile `id` with epilogue `epi`; `vec` selects the 16-byte-aligned load path.

@@ -5,13 +5,20 @@ The paper tunes its kernel per (M, N, K) with an autotuner over 36 configuration
 first call (Section 3, "Why autotuning is load-bearing"); here the search runs once,
 offline, on the target GPU, and its result is a constant table in the library.
 
-Usage (on an MI355X): python -m paper_2606_14598_amd.tune --out tile_table.inc [--json r.json]
+Two sets of shapes: the workload shapes (one entry each, for their exact M) and the
+paper's five model shapes over its token counts (Section 3, "Target architecture";
+Section 5), which get token-count buckets: each swept M owns the range up to the
+midpoints with its neighbours.
+
+Usage (on an MI355X): python -m paper_2606_14598_amd.tune --out tile_table.inc
+       [--json r.json] [--set all|workloads|paper] [--iters N]
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import re
 import sys
 
 import numpy as np
@@ -26,8 +33,11 @@ import synth_inputs as si  # noqa: E402
 
 HEADER = """// Offline-chosen GEMM tile per shape: {M lower bound, M upper bound, N, K, tile id}.
 // Written by paper_2606_14598_amd/tune.py from a timed sweep of every tile on MI355X;
-// shapes not listed use the fallback rule in gemm_i8.hip.
+// shapes not listed use the fallback rule in gemm_i8.hip, whose cost model takes each
+// tile's sustained rate from kTileRate below.
 """
+
+CUS = 256
 
 
 def time_ms(fn, iters=20, warmup=3):
@@ -54,50 +64,102 @@ def time_ms(fn, iters=20, warmup=3):
     return st.elapsed_time(en) / (3 * iters)
 
 
-def shapes():
+def shapes(which: str = "all"):
+    """(shape, M lower bound, M upper bound) of every entry to tune."""
     seen = set()
-    for c in sorted(si.WORKLOADS):
-        for s in si.WORKLOADS[c]:
-            key = (s.M, s.N, s.K)
-            if key not in seen:
-                seen.add(key)
-                yield s
+    if which in ("all", "workloads"):
+        for c in sorted(si.WORKLOADS):
+            for s in si.WORKLOADS[c]:
+                key = (s.M, s.N, s.K)
+                if key not in seen:
+                    seen.add(key)
+                    yield s, s.M, s.M
+    if which in ("all", "paper"):
+        ms = sorted(si.PAPER_M)
+        for name, _, _ in si.PAPER_SHAPES:
+            for i, M in enumerate(ms):
+                lo = 257 if i == 0 else (ms[i - 1] + M) // 2 + 1
+                hi = (1 << 62) if i == len(ms) - 1 else (M + ms[i + 1]) // 2
+                yield si.paper_shape(name, M), lo, hi
 
 
 def _dev_bf16(bits, dev):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
 
 
-def sweep(iters: int):
-    """Time every tile on every workload shape, on the workload's own synthetic inputs
-    quantized by the library: the matrix cores' sustained rate depends on the operand
-    bits (switching power), so uniform random or constant codes would mislead."""
+def sweep(iters: int, which: str = "all"):
+    """Time every tile on every shape, on the shape's own synthetic inputs quantized by
+    the library: the matrix cores' sustained rate depends on the operand bits
+    (switching power), so uniform random or constant codes would mislead. The
+    weight-streaming tiles (made for M <= 128) are skipped above 128 tokens."""
     dev = torch.device("cuda:0")
     results = []
-    for s in shapes():
+    for s, lo, hi in shapes(which):
         x, w, bb = si.make_inputs(s)
-        xq, sx = w8a8.quantize_act(_dev_bf16(x, dev))
+        xd = _dev_bf16(x, dev)
+        del x
+        xq, sx = w8a8.quantize_act(xd)
+        del xd
         wq, sw = w8a8.quantize_weight(_dev_bf16(w, dev))
         b = _dev_bf16(bb, dev)
-        row = {"M": s.M, "N": s.N, "K": s.K, "ms": {}}
+        row = {"name": s.name, "M": s.M, "N": s.N, "K": s.K, "m_lo": lo, "m_hi": hi,
+               "default": w8a8.tile_name(w8a8.default_tile(s.M, s.N, s.K)), "ms": {}}
         y = torch.empty((s.M, s.N), dtype=torch.bfloat16, device=dev)
+        it = iters if s.ops < 5e14 else max(3, iters // 4)
         for t in range(w8a8.tile_count()):
-            ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t, out=y), iters)
-            row["ms"][w8a8.tile_name(t)] = ms
+            name = w8a8.tile_name(t)
+            if s.M > 128 and name.startswith("skinny"):
+                continue
+            ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t, out=y), it)
+            row["ms"][name] = ms
         best = min(row["ms"], key=row["ms"].get)
         row["best"] = best
         row["best_tops"] = 2 * s.M * s.N * s.K / (row["ms"][best] * 1e-3) / 1e12
         print(json.dumps(row), flush=True)
         results.append(row)
+        del xq, sx, wq, sw, b, y
+        torch.cuda.empty_cache()
     return results
+
+
+def _tile_dims(name):
+    m = re.match(r"m(\d+)n(\d+)k(\d+)", name)
+    return tuple(int(g) for g in m.groups()) if m else None
+
+
+def tile_rates(results, names):
+    """Sustained TOP/s of each LDS-staged tile: the median over swept shapes with at least
+    512 tokens of its achieved rate divided by its wave efficiency (tiles / (waves *
+    CUs)), i.e. what it would reach with every CU busy. 0 for the weight-streaming tiles
+    (not modeled)."""
+    per = {n: [] for n in names}
+    for r in results:
+        if r["M"] < 512:
+            continue
+        for n, ms in r["ms"].items():
+            d = _tile_dims(n)
+            if d is None:
+                continue
+            tiles = -(-r["M"] // d[0]) * -(-r["N"] // d[1])
+            waves = -(-tiles // CUS)
+            per[n].append(2 * r["M"] * r["N"] * r["K"] / (ms * 1e-3) / 1e12
+                          / (tiles / (waves * CUS)))
+    return [float(np.median(per[n])) if per[n] else 0.0 for n in names]
 
 
 def write_table(results, path):
     names = [w8a8.tile_name(t) for t in range(w8a8.tile_count())]
-    lines = [HEADER, "static const TableEntry kTileTable[] = {"]
+    rates = tile_rates(results, names)
+    lines = [HEADER, "static const float kTileRate[] = {"]
+    for n, v in zip(names, rates):
+        lines.append(f"    {v:.0f}.0f,  // {n}")
+    lines.append("};")
+    lines.append("")
+    lines.append("static const TableEntry kTileTable[] = {")
     for r in results:
-        lines.append(f"    {{{r['M']}, {r['M']}, {r['N']}, {r['K']}, {names.index(r['best'])}}},"
-                     f"  // {r['best']} {r['best_tops']:.0f} TOPS")
+        lines.append(f"    {{{r['m_lo']}, {r['m_hi']}, {r['N']}, {r['K']}, "
+                     f"{names.index(r['best'])}}},  // M={r['M']} {r['best']} "
+                     f"{r['best_tops']:.0f} TOPS")
     lines.append("    {0, 0, 0, 0, -1},  // sentinel")
     lines.append("};")
     with open(path, "w") as f:
@@ -109,10 +171,19 @@ def main():
     ap.add_argument("--out", required=True)
     ap.add_argument("--json")
     ap.add_argument("--iters", type=int, default=20)
+    ap.add_argument("--set", default="all", choices=["all", "workloads", "paper"])
+    ap.add_argument("--from-json", help="rewrite the table from a saved sweep (no timing)")
     a = ap.parse_args()
-    res = sweep(a.iters)
+    if a.from_json:
+        with open(a.from_json) as f:
+            res = json.load(f)
+        for r in res:
+            r.setdefault("m_lo", r["M"])
+            r.setdefault("m_hi", r["M"])
+    else:
+        res = sweep(a.iters, a.set)
     write_table(res, a.out)
-    if a.json:
+    if a.json and not a.from_json:
         with open(a.json, "w") as f:
             json.dump(res, f, indent=1)
 

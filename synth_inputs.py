@@ -35,8 +35,8 @@ import math
 
 import numpy as np
 
-__all__ = ["Shape", "WORKLOADS", "make_inputs", "workload", "shape_seed",
-           "bf16_bits_from_f32"]
+__all__ = ["Shape", "WORKLOADS", "PAPER_SHAPES", "PAPER_M", "paper_shape", "make_inputs",
+           "workload", "shape_seed", "bf16_bits_from_f32"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -82,6 +82,27 @@ WORKLOADS = {
                for M in (1, 77, 333, 4625) for N in (4096, 16384)]
            + [(f"m{M}_k3136", M, 3136, 4096, "student_t") for M in (1, 77, 333, 4625)]),
 }
+
+
+# The paper's own model: five distinct GEMM shapes (name, N, K) of its 4608-wide DiT
+# (Section 3, "Target architecture"), timed over the token counts of its speedup claim,
+# M = 512 .. 16384, which contain the in-model M ~ 4110 at 1024px (Section 5, "The
+# kernel is exact and the GEMMs are compute-bound"). The down-projection reads a GELU
+# output, the others outlier-channel activations.
+PAPER_SHAPES = [("qkv", 13824, 4608), ("attn_out", 4608, 4608), ("ffn_up", 12288, 4608),
+                ("ffn_down", 4608, 12288), ("llm_proj", 4608, 53248)]
+PAPER_M = [512, 1024, 2048, 4096, 4110, 8192, 16384]
+
+
+def paper_shape(name: str, M: int) -> Shape:
+    """The paper shape `name` at M tokens (seed 20260 + 500 + 10 * shape + M index, M
+    indexed in PAPER_M or appended after it)."""
+    names = [p[0] for p in PAPER_SHAPES]
+    i = names.index(name)
+    _, N, K = PAPER_SHAPES[i]
+    j = PAPER_M.index(M) if M in PAPER_M else len(PAPER_M)
+    return Shape(name, M, K, N, "gelu" if name == "ffn_down" else "outlier",
+                 shape_seed(5, 10 * i + j))
 
 
 def workload(config: int, name: str) -> Shape:

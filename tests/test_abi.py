@@ -159,3 +159,39 @@ def test_python_binding_checks_transform_arguments():
         w8a8.quantize_act(x, act="relu")
     with pytest.raises(ValueError):
         w8a8.col_absmax(x, accumulate=True)
+
+
+def _table_rates():
+    path = os.path.join(ROOT, "paper_2606_14598_amd", "csrc", "tile_table.inc")
+    text = open(path).read()
+    body = text[text.index("kTileRate[] = {"):]
+    body = body[:body.index("};")]
+    return [float(v) for v in re.findall(r"([0-9.]+)f,", body)]
+
+
+def test_default_tile_follows_the_wave_cost_model(lib):
+    rates = _table_rates()
+    n = lib.w8a8_tile_count()
+    assert len(rates) == n
+    dims = []
+    for i in range(n):
+        m = re.match(r"m(\d+)n(\d+)", lib.w8a8_tile_name(i).decode())
+        dims.append((int(m.group(1)), int(m.group(2))) if m else None)
+    for M, N, K in [(129, 4096, 4096), (333, 16384, 4096), (512, 4608, 4608),
+                    (2560, 4096, 4096), (4110, 13824, 4608), (5000, 7000, 4096),
+                    (16384, 4608, 53248)]:
+        best, cost = None, None
+        for i in range(n):
+            if rates[i] <= 0:
+                continue
+            tm, tn = dims[i]
+            rounds = -(-(-(-M // tm) * -(-N // tn)) // 256)
+            c = rounds * tm * tn / rates[i]
+            if cost is None or c < cost:
+                best, cost = i, c
+        assert lib.w8a8_default_tile(M, N, K) == best, (M, N, K)
+    # few tokens: weight-streaming tiles
+    for M in (1, 16, 64, 128):
+        name = lib.w8a8_tile_name(lib.w8a8_default_tile(M, 128, 4096)).decode()
+        assert name.startswith("skinny"), (M, name)
+    assert lib.w8a8_default_tile(0, 8, 8) == -1
