@@ -1,0 +1,72 @@
+"""The torch.library registration: schemas and fake (meta) implementations on the CPU,
+real calls, opcheck and torch.compile without graph breaks on the GPU."""
+import pytest
+import torch
+from torch._subclasses.fake_tensor import FakeTensorMode
+
+import paper_2606_14598_amd as w8a8
+import paper_2606_14598_amd.torch_ops as ops
+
+
+def test_ops_are_registered():
+    for name in ("linear", "quantize_act", "gemm"):
+        assert hasattr(torch.ops.w8a8, name)
+
+
+def test_fake_shapes_and_dtypes():
+    with FakeTensorMode():
+        x = torch.empty(2, 77, 4096, dtype=torch.bfloat16, device="cuda")
+        wq = torch.empty(12288, 4096, dtype=torch.int8, device="cuda")
+        sw = torch.empty(12288, dtype=torch.float32, device="cuda")
+        b = torch.empty(12288, dtype=torch.bfloat16, device="cuda")
+        y = torch.ops.w8a8.linear(x, wq, sw, b, 1, None)
+        assert y.shape == (2, 77, 12288) and y.dtype == torch.bfloat16
+        x2 = torch.empty(154, 4096, dtype=torch.bfloat16, device="cuda")
+        xq, sx = torch.ops.w8a8.quantize_act(x2, 0, None)
+        assert xq.shape == (154, 4096) and xq.dtype == torch.int8
+        assert sx.shape == (154,) and sx.dtype == torch.float32
+        y2 = torch.ops.w8a8.gemm(xq, sx, wq, sw, None)
+        assert y2.shape == (154, 12288) and y2.dtype == torch.bfloat16
+
+
+@pytest.mark.gpu
+def test_module_and_compile_without_graph_breaks():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.manual_seed(0)
+    lin1 = torch.nn.Linear(1024, 2048).cuda().to(torch.bfloat16)
+    lin2 = torch.nn.Linear(2048, 512).cuda().to(torch.bfloat16)
+    m1 = ops.W8A8Linear.from_linear(lin1)
+    m2 = ops.W8A8Linear.from_linear(lin2, act="gelu")
+
+    def block(x):
+        return m2(m1(x)) + 1.0
+
+    x = torch.randn(3, 100, 1024, device="cuda", dtype=torch.bfloat16)
+    eager = block(x)
+    # the module path is the library path
+    h = w8a8.linear(x, m1.wq, m1.w_scale, m1.bias)
+    assert torch.equal(eager, w8a8.linear(h, m2.wq, m2.w_scale, m2.bias, act="gelu") + 1.0)
+    explained = torch._dynamo.explain(block)(x)
+    assert explained.graph_break_count == 0, explained.break_reasons
+    compiled = torch.compile(block, fullgraph=True, backend="aot_eager")
+    assert torch.equal(compiled(x), eager)
+
+
+@pytest.mark.gpu
+def test_opcheck():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    x = torch.randn(33, 256, device="cuda", dtype=torch.bfloat16)
+    w = torch.randn(64, 256, device="cuda", dtype=torch.bfloat16)
+    wq, sw = w8a8.quantize_weight(w)
+    b = torch.randn(64, device="cuda", dtype=torch.bfloat16)
+    cm = torch.rand(256, device="cuda") + 0.5
+    tests = ("test_schema", "test_faketensor")
+    torch.library.opcheck(torch.ops.w8a8.linear.default, (x, wq, sw, b, 0, None),
+                          test_utils=tests)
+    torch.library.opcheck(torch.ops.w8a8.linear.default, (x, wq, sw, None, 1, cm),
+                          test_utils=tests)
+    torch.library.opcheck(torch.ops.w8a8.quantize_act.default, (x, 1, cm), test_utils=tests)
+    xq, sx = w8a8.quantize_act(x)
+    torch.library.opcheck(torch.ops.w8a8.gemm.default, (xq, sx, wq, sw, b), test_utils=tests)
