@@ -2,7 +2,9 @@
 
 One step is one pass of the hot path over one batch: per-token int8 quantization of the
 activations, then the int8 GEMM with the fused dequantization + bias epilogue (the weight
-is quantized once, before timing: it is an offline step). The workload is the DiT
+is quantized once, before timing: it is an offline step). The default 400 warm-up steps
+(~20 ms) let the chip's power management settle: under sustained int8 MFMA load the
+step time dips for ~15 ms after a start or an idle gap before it becomes steady. The workload is the DiT
 attention-projection linear of a 768px-like sequence: M = 2560 tokens (2304 image + 256
 text), K = 4096, N = 4096, synthetic seeded bf16 inputs.
 
@@ -355,9 +357,11 @@ def run(args) -> dict:
 FIXED_TILE = 0   # one configuration for every shape: the untuned-by-design arm
 
 
-def graph_ms(fn, iters: int = 20) -> float:
-    """Mean ms per call of fn, `iters` calls captured in one HIP graph and replayed (no
-    host launch overhead in the measurement, which matters for microsecond shapes)."""
+def graph_ms(fn, iters: int = 20, warm_ms: float = 25.0, min_timed_ms: float = 3.0) -> float:
+    """Mean ms per call of fn: `iters` calls captured in one HIP graph (no host launch
+    overhead in the measurement, which matters for microsecond shapes), replayed until
+    `warm_ms` of sustained work has run (the power management of the chip settles only
+    after ~15-20 ms of load), then timed over enough replays to cover `min_timed_ms`."""
     import torch
     for _ in range(3):
         fn()
@@ -368,15 +372,23 @@ def graph_ms(fn, iters: int = 20) -> float:
         with torch.cuda.graph(g, stream=s):
             for _ in range(iters):
                 fn()
-    g.replay()
-    torch.cuda.synchronize()
     st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     st.record()
-    for _ in range(3):
+    g.replay()
+    en.record()
+    torch.cuda.synchronize()
+    once = max(st.elapsed_time(en), 1e-3)
+    for _ in range(int(warm_ms / once) + 1):
+        g.replay()
+    reps = max(3, int(min_timed_ms / once) + 1)
+    torch.cuda.synchronize()
+    st.record()
+    for _ in range(reps):
         g.replay()
     en.record()
     torch.cuda.synchronize()
-    return st.elapsed_time(en) / (3 * iters)
+    return st.elapsed_time(en) / (reps * iters)
 
 
 def all_shapes(args):
@@ -608,8 +620,10 @@ def copy_calibration():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=400,
+                    help="untimed steps first: the chip's power management settles only "
+                         "after ~15-20 ms of sustained int8 MFMA load")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-extra", action="store_true",
                     help="only the timed step (health gate, comparators, variant skipped)")

@@ -30,6 +30,7 @@ namespace {
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Buffer-resource word 3 for gfx9 (raw 32-bit data format, no swizzle).
 constexpr int kRsrcWord3 = 0x00020000;
@@ -224,8 +225,12 @@ __device__ __forceinline__ void store_tile_bf16_lds(const i32x16 (&acc)[FN][FM],
             const uint4 v = *reinterpret_cast<const uint4 *>(region + row * RS + ch * 16);
             const int64_t mm = m_base + j * 32 + row;
             const int64_t nn = n_base + ch * 8;
+            // Streaming (nontemporal) stores: the output is not read again by this
+            // kernel, and lines that bypass the L2's write-back set leave less to flush
+            // when the kernel ends.
             if (mm < M && nn < N)
-                *reinterpret_cast<uint4 *>(out + mm * N + nn) = v;
+                __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w},
+                                            reinterpret_cast<u32x4 *>(out + mm * N + nn));
         }
     }
 }

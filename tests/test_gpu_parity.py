@@ -298,3 +298,38 @@ def test_full_size_sampled(config, name):
     assert np.array_equal(host(acc)[:, cols], acc_c)
     st2 = assert_bf16_parity(y[:, cols], y_c, f"{name} cols")
     say("   rows", st, "cols", st2)
+
+
+# ---------------------------------------------------------------- HIP graphs
+
+@pytest.mark.parametrize("act,with_cm", [("none", False), ("gelu", True)])
+def test_graph_replays_match_eager(act, with_cm):
+    """The entry points allocate nothing and record no memset, so a captured linear
+    replays correctly: several replays, with eager work and synchronizations between
+    them, each equal bit for bit to the eager result."""
+    M, K, N = 2560, 4096, 4096
+    x, w, b = si.make_inputs((M, K, N), seed=20360)
+    xd, bd = dev_bf16(x), dev_bf16(b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    cm = torch.rand(K, device="cuda") + 0.5 if with_cm else None
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8, device="cuda")
+    want = host_bits(w8a8.linear(xd, wq, sw, bd, act=act, col_mul=cm))
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            w8a8.linear(xd, wq, sw, bd, act=act, col_mul=cm, out=y, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    other = torch.empty_like(y)
+    for r in range(4):
+        y.zero_()
+        ws.fill_(0x5A)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(host_bits(y), want), f"replay {r}"
+        # eager work between replays, through the same workspace
+        w8a8.linear(xd[: M // 2], wq, sw, None, out=other[: M // 2], workspace=ws)
+        torch.cuda.synchronize()
