@@ -484,6 +484,23 @@ gemm_i8_lds_kernel(KParams kp) {
                 __builtin_amdgcn_s_waitcnt(waitcnt_vm(Y * (NV - 1)));
         }
     };
+    // Before the last K-step of panel kt (S >= 3): panel kt+1 has landed once at most the
+    // full panels kt+2 .. kt+S-2 and the slices of panel kt+S-1 issued so far (K-steps
+    // 0 .. KS-2) are in flight. A wavefront with one load fewer skips the last slot.
+    auto wait_loads_mid = [&]() {
+        constexpr int VPS_ = (NV + KS - 1) / KS;
+        constexpr int ISS = (KS - 1) * VPS_ < NV ? (KS - 1) * VPS_ : NV;
+        constexpr int ISS1 = (KS - 1) * VPS_ < NV - 1 ? (KS - 1) * VPS_ : NV - 1;
+        static_assert(S < 3 || (S - 3) * NV + ISS <= 63, "vmcnt range");
+        if constexpr (NI % NW == 0) {
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 3) * NV + ISS));
+        } else {
+            if (wave < NI % NW)
+                __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 3) * NV + ISS));
+            else
+                __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 3) * (NV - 1) + ISS1));
+        }
+    };
 
     i32x4 fa[2][FN], fb[2][FM];
     auto read_frags = [&](int so, int ks, int buf) {
@@ -502,17 +519,27 @@ gemm_i8_lds_kernel(KParams kp) {
     // then its share of the loads of panel k+S-1, each followed by one MFMA, with a
     // scheduling fence around every pair. The matrix core then always has an MFMA
     // queued while a memory instruction issues.
+    //
+    // With three or more stages (EARLY) the per-panel wait and barrier come one K-step
+    // before the panel ends, and the last K-step reads the first fragments of the next
+    // panel (from stage so_rd), so their LDS latency hides behind its MFMAs instead of
+    // stalling the first MFMA of every panel. With two stages the next panel is still
+    // being loaded during the last K-step, so the barrier stays at the panel's end.
     constexpr int NM = FN * FM, NR = FN + FM;
     constexpr int VPS = (NV + KS - 1) / KS;   // loads per K-step
-    auto kstep = [&](auto ksc, int so, int kt_load, int so_load) {
+    constexpr bool EARLY = S >= 3;
+    static_assert(KS % 2 == 0, "fragment double buffer: K-step 0 of a panel uses buffer 0");
+    auto kstep = [&](auto ksc, int so, int kt_load, int so_load, int so_rd) {
         constexpr int ks = decltype(ksc)::value;
-        constexpr int nr = ks + 1 < KS ? NR : 0;
+        constexpr bool next_panel = EARLY && ks + 1 == KS;
+        constexpr int nr = (ks + 1 < KS || next_panel) ? NR : 0;
+        constexpr int fk = ks + 1 < KS ? ks + 1 : 0;
         constexpr int va = ks * VPS < NV ? ks * VPS : NV;
         constexpr int vb = (ks + 1) * VPS < NV ? (ks + 1) * VPS : NV;
         constexpr int nops = nr + (vb - va);
         constexpr int steps = NM > nops ? NM : nops;
-        const int8_t *sw_ = smem + so + wn * WTN * BK + fofs[ks + 1 < KS ? ks + 1 : 0];
-        const int8_t *sx_ = smem + so + TN * BK + wm * WTM * BK + fofs[ks + 1 < KS ? ks + 1 : 0];
+        const int8_t *sw_ = smem + so_rd + wn * WTN * BK + fofs[fk];
+        const int8_t *sx_ = smem + so_rd + TN * BK + wm * WTM * BK + fofs[fk];
         [&]<int... q>(std::integer_sequence<int, q...>) {
             ([&] {
                 if constexpr (q < nr) {
@@ -586,19 +613,43 @@ gemm_i8_lds_kernel(KParams kp) {
         barrier_nofence();
         int st = 0;            // stage of panel kt
         int ld = S - 1;        // stage of panel kt + S - 1
-        for (int kt = 0; kt < nk; ++kt) {
-            read_frags(st * STAGE, 0, 0);
+        if constexpr (EARLY) {
+            read_frags(0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
-            [&]<int... ks>(std::integer_sequence<int, ks...>) {
-                (kstep(std::integral_constant<int, ks>{}, st * STAGE, kt + S - 1, ld * STAGE), ...);
-            }(std::make_integer_sequence<int, KS>{});
-            // Panel kt+1 has landed once at most the S-2 younger panels are in flight.
-            wait_loads(std::integral_constant<int, S - 2>{});
-            barrier_nofence();
-            st = (st + 1 == S) ? 0 : st + 1;
+        }
+        for (int kt = 0; kt < nk; ++kt) {
+            const int nx = (st + 1 == S) ? 0 : st + 1;
+            if constexpr (EARLY) {
+                [&]<int... ks>(std::integer_sequence<int, ks...>) {
+                    (kstep(std::integral_constant<int, ks>{}, st * STAGE, kt + S - 1, ld * STAGE,
+                           st * STAGE), ...);
+                }(std::make_integer_sequence<int, KS - 1>{});
+                // Panel kt+1 is in LDS for every wavefront after this barrier. The
+                // lgkmcnt(0) first: this wavefront's reads of panel kt's stage are done
+                // before anyone can pass the barrier and, one panel later, refill it.
+                wait_loads_mid();
+                __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+                barrier_nofence();
+                kstep(std::integral_constant<int, KS - 1>{}, st * STAGE, kt + S - 1,
+                      ld * STAGE, nx * STAGE);
+            } else {
+                read_frags(st * STAGE, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                [&]<int... ks>(std::integer_sequence<int, ks...>) {
+                    (kstep(std::integral_constant<int, ks>{}, st * STAGE, kt + S - 1,
+                           ld * STAGE, st * STAGE), ...);
+                }(std::make_integer_sequence<int, KS>{});
+                // Panel kt+1 has landed once at most the S-2 younger panels are in flight.
+                wait_loads(std::integral_constant<int, S - 2>{});
+                barrier_nofence();
+            }
+            st = nx;
             ld = (ld + 1 == S) ? 0 : ld + 1;
         }
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // the zero-filling tail loads
+        // The zero-filling tail loads, and (S >= 3) the last K-step's reads of the stage
+        // after the final panel, whose data nobody uses.
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        __builtin_amdgcn_s_waitcnt(0xC07F);
     } else {
         park_vectors();
     }
