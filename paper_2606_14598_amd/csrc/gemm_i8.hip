@@ -889,6 +889,13 @@ const TileEntry kTiles[] = {
     W8A8_SKINNY("skinny_m16n64w16", 1, 4, 16),
     W8A8_SKINNY("skinny_m64n32w16", 4, 2, 16),
     W8A8_SKINNY("skinny_m128n32w8", 8, 2, 8),
+    // Few tokens (a few hundred): small tiles with deep rings keep enough bytes in flight
+    // per CU for the panel loads, which their little MFMA work per panel cannot hide.
+    W8A8_TILE("m128n128k128w2x2s4", 128, 128, 128, 2, 2, 8, 4),
+    W8A8_TILE("m64n128k128w1x4s6", 64, 128, 128, 1, 4, 8, 6),
+    W8A8_TILE("m32n128k128w1x4s6", 32, 128, 128, 1, 4, 8, 6),
+    W8A8_TILE("m64n64k128w2x2s8", 64, 64, 128, 2, 2, 8, 8),
+    W8A8_TILE("m64n64k128w1x2s8", 64, 64, 128, 1, 2, 8, 8),
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
