@@ -83,6 +83,11 @@ w8a8_status w8a8_gemm(const int8_t *xq, const float *x_scale, const int8_t *wq,
 
 size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
+/* Workspace of w8a8_gemm_ex with a given tile id (-1: the table's choice). Tiles that
+ * split K among several workgroups per output tile keep int32 partial products
+ * [splits][M][N] there; the others need none (0). */
+size_t w8a8_gemm_workspace_bytes_ex(int64_t M, int64_t N, int64_t K, int tile_id);
+
 /* The whole quantized linear: per-token quantization of x into the workspace, then the
  * fused GEMM (steps 2 and 3). wq / w_scale come from w8a8_quantize_weight.
  * workspace: at least w8a8_linear_workspace_bytes(M,N,K) bytes, 256-byte aligned; it
@@ -107,7 +112,10 @@ w8a8_status w8a8_gemm_acc_i32(const int8_t *xq, const int8_t *wq, int32_t *acc,
  * w8a8_default_tile returns the fallback rule's choice alone, the untuned arm of the
  * tuning ablation. Both return -1 for M <= 0, N <= 0 or K < 0. The _ex variants run a
  * given id (-1 = the table's choice) for offline sweeps and tests. An id outside
- * [0, w8a8_tile_count()) returns W8A8_ERR_ARG. */
+ * [0, w8a8_tile_count()) returns W8A8_ERR_ARG. Tiles whose name ends in _k<s> divide K
+ * among s workgroups per output tile and sum the int32 partials in a second kernel (the
+ * result is the same: integer sums are exact); w8a8_gemm_acc_i32[_ex] runs them
+ * unsplit. */
 int w8a8_tile_count(void);
 const char *w8a8_tile_name(int tile_id);
 int w8a8_select_tile(int64_t M, int64_t N, int64_t K);

@@ -73,6 +73,7 @@ def load_library():
         "w8a8_gemm": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
         "w8a8_gemm_ex": ([P, P, P, P, P, P, I64, I64, I64, P, SZ, INT, P], INT),
         "w8a8_gemm_workspace_bytes": ([I64, I64, I64], SZ),
+        "w8a8_gemm_workspace_bytes_ex": ([I64, I64, I64, INT], SZ),
         "w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
         "w8a8_linear_workspace_bytes": ([I64, I64, I64], SZ),
         "w8a8_gemm_acc_i32": ([P, P, P, I64, I64, I64, P], INT),
@@ -150,8 +151,8 @@ def default_tile(M: int, N: int, K: int) -> int:
     return int(load_library().w8a8_default_tile(M, N, K))
 
 
-def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
-    return int(load_library().w8a8_gemm_workspace_bytes(M, N, K))
+def gemm_workspace_bytes(M: int, N: int, K: int, tile: int = -1) -> int:
+    return int(load_library().w8a8_gemm_workspace_bytes_ex(M, N, K, int(tile)))
 
 
 def linear_workspace_bytes(M: int, N: int, K: int) -> int:
@@ -270,7 +271,7 @@ def gemm(xq, x_scale, wq, w_scale, bias=None, *, tile: int = -1, out=None,
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
                                                 device=xq.device)
     _check(y, torch.bfloat16, 2, "out")
-    ws = _workspace(gemm_workspace_bytes(M, N, K), xq.device, workspace)
+    ws = _workspace(gemm_workspace_bytes(M, N, K, tile), xq.device, workspace)
     nws = 0 if ws is None else ws.numel() * ws.element_size()
     with torch.cuda.device(xq.device):
         _call("w8a8_gemm_ex", _ptr(xq), _ptr(x_scale), _ptr(wq), _ptr(w_scale), _ptr(bias),

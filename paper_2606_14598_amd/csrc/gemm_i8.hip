@@ -96,6 +96,10 @@ struct KParams {
     int gm;          // token-tiles per raster group
     int out_vec;     // 0: scalar stores; 1: rows 8-byte (bf16) / 16-byte (int32) aligned
                      // with N % 4 == 0; 2 (bf16): rows 16-byte aligned with N % 8 == 0
+    int k_split;     // workgroups per output tile along K (1: the whole K, direct epilogue)
+    int k_chunk;     // K bytes per split (a multiple of BK; K when unsplit)
+    int part_vec;    // partial rows 16-byte aligned (N % 4 == 0)
+    int32_t *part;   // k_split > 1: int32 partials [k_split][M][N]
 };
 
 // Epilogue of one wavefront's (FN*32 channels) x (FM*32 tokens) accumulator tile whose
@@ -405,17 +409,26 @@ gemm_i8_lds_kernel(KParams kp) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave % WM, wn = wave / WM;
+    // Split-K: workgroup b works on K-range `split` of tile b mod (tiles_m * tiles_n).
+    int blk = blockIdx.x, split = 0;
+    if (kp.k_split > 1) {
+        const int ntiles = kp.tiles_m * kp.tiles_n;
+        split = blk / ntiles;
+        blk -= split * ntiles;
+    }
     int tm, tn;
-    tile_of(blockIdx.x, kp.tiles_m, kp.tiles_n, kp.gm, tm, tn);
+    tile_of(blk, kp.tiles_m, kp.tiles_n, kp.gm, tm, tn);
     const int64_t m0 = (int64_t)tm * TM, n0 = (int64_t)tn * TN;
     const int64_t M = a.M, N = a.N;
-    const int K = (int)a.K;
+    const int K = (int)a.K;                              // row stride of Xq and Wq
+    const int kbeg = split * kp.k_chunk;                 // this workgroup's first K byte
+    const int KL = (K - kbeg) < kp.k_chunk ? (K - kbeg) : kp.k_chunk;   // its K length
     const int rows_w = (int)((N - n0) < TN ? (N - n0) : TN);
     const int rows_x = (int)((M - m0) < TM ? (M - m0) : TM);
     const __amdgpu_buffer_rsrc_t rw_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(a.wq + n0 * K), (short)0, rows_w * K, kRsrcWord3);
+        (void *)(a.wq + n0 * K + kbeg), (short)0, rows_w * K - kbeg, kRsrcWord3);
     const __amdgpu_buffer_rsrc_t rx_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(a.xq + m0 * K), (short)0, rows_x * K, kRsrcWord3);
+        (void *)(a.xq + m0 * K + kbeg), (short)0, rows_x * K - kbeg, kRsrcWord3);
 
     // Load instruction g (0 <= g < NI; the first IW fill the weight part of a stage, the
     // rest the activation part) is issued by wavefront g % NW; its lane l fills LDS chunk
@@ -440,7 +453,7 @@ gemm_i8_lds_kernel(KParams kp) {
         for (int j = 0; j < FM; ++j)
             acc[i][j] = i32x16{};
 
-    const int nk = (K + BK - 1) / BK;
+    const int nk = (KL + BK - 1) / BK;
 
     // Loads [I0, I1) of this wavefront's NV load instructions of panel kt into the stage
     // at byte offset so. Only the last panel can reach past K; there, lanes whose chunk
@@ -450,7 +463,7 @@ gemm_i8_lds_kernel(KParams kp) {
     auto issue = [&](auto i0c, auto i1c, int kt, int so) {
         constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
         const int k0 = kt * BK;
-        const bool full = (kt < nk) & (k0 + BK <= K);
+        const bool full = (kt < nk) & (k0 + BK <= KL);
         const bool inrange = kt < nk;
 #pragma unroll
         for (int i = I0; i < I1; ++i) {
@@ -461,7 +474,7 @@ gemm_i8_lds_kernel(KParams kp) {
             const int gg = isw ? g : g - IW;
             const int row = gg * RPI + lrow;
             const int kc = lchunk ^ swz<BK>(row);
-            const bool ok = full | (inrange & (k0 + kc * 16 < K));
+            const bool ok = full | (inrange & (k0 + kc * 16 < KL));
             const int off = ok ? row * K + k0 + kc * 16 : kOOB;
             int8_t *dst = smem + so + (isw ? 0 : TN * BK) + gg * 1024;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -653,6 +666,15 @@ gemm_i8_lds_kernel(KParams kp) {
     } else {
         park_vectors();
     }
+    if (kp.k_split > 1) {
+        // Split-K: store this K-range's int32 partial; the reduce kernel sums the splits
+        // and runs the epilogue.
+        KParams kq = kp;
+        kq.a.out = kp.part + (int64_t)split * M * N;
+        kq.out_vec = kp.part_vec;
+        store_tile<FN, FM, EPI_I32>(acc, kq, m0 + wm * WTM, n0 + wn * WTN, lane);
+        return;
+    }
     if constexpr (EPI == EPI_BF16) {
         static_assert(NW * 32 * (2 * WTN + 16) <= S * STAGE, "epilogue staging");
         if (kp.out_vec == 2) {
@@ -789,6 +811,65 @@ gemm_i8_skinny_kernel(KParams kp) {
 
 // ---------------------------------------------------------------- tile registry
 
+// Split-K reduction and epilogue: acc = sum of the k_split int32 partials (exact in any
+// order), then the same epilogue as the tiled kernels, y = bf16(fmaf(float(acc),
+// sx[m] * sw[n], b[n])), or the int32 sum itself. Four channels per thread when the
+// partial rows are 16-byte aligned, one otherwise.
+template <int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(KParams kp) {
+    const GemmArgs &a = kp.a;
+    const int64_t M = a.M, N = a.N, MN = M * N;
+    const int S = kp.k_split;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (kp.part_vec) {
+        const int64_t nq = N / 4;
+        if (t >= M * nq)
+            return;
+        const int64_t m = t / nq, n = (t - m * nq) * 4;
+        const int32_t *p = kp.part + m * N + n;
+        i32x4 acc = *reinterpret_cast<const i32x4 *>(p);
+        for (int sp = 1; sp < S; ++sp)
+            acc += *reinterpret_cast<const i32x4 *>(p + sp * MN);
+        if constexpr (EPI == EPI_I32) {
+            *reinterpret_cast<i32x4 *>(static_cast<int32_t *>(a.out) + m * N + n) = acc;
+        } else {
+            const float sxm = a.sx[m];
+            uint16_t h[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float b = a.bias ? __uint_as_float((uint32_t)a.bias[n + e] << 16) : 0.0f;
+                const float y = __builtin_fmaf((float)acc[e], sxm * a.sw[n + e], b);
+                h[e] = __builtin_bit_cast(uint16_t, (__bf16)y);
+            }
+            uint16_t *o = static_cast<uint16_t *>(a.out) + m * N + n;
+            if (kp.out_vec) {
+                uint2 pk;
+                pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+                pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+                *reinterpret_cast<uint2 *>(o) = pk;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    o[e] = h[e];
+            }
+        }
+    } else {
+        if (t >= MN)
+            return;
+        const int64_t m = t / N, n = t - m * N;
+        int32_t acc = kp.part[t];
+        for (int sp = 1; sp < S; ++sp)
+            acc += kp.part[t + sp * MN];
+        if constexpr (EPI == EPI_I32) {
+            static_cast<int32_t *>(a.out)[t] = acc;
+        } else {
+            const float b = a.bias ? __uint_as_float((uint32_t)a.bias[n] << 16) : 0.0f;
+            const float y = __builtin_fmaf((float)acc, a.sx[m] * a.sw[n], b);
+            static_cast<uint16_t *>(a.out)[t] = __builtin_bit_cast(uint16_t, (__bf16)y);
+        }
+    }
+}
+
 template <int TM, int TN, int BK, int WM, int WN, int S>
 struct Tile {
     // S >= 2: pipelined direct-to-LDS kernel with S stages; S == 0: the simple
@@ -800,7 +881,7 @@ struct Tile {
     // Aligned operands only (16-byte pointers, K % 16 == 0); launch_gemm sends the rest
     // to the generic tile.
     static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
-        const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n)), block(threads);
+        const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n * kp.k_split)), block(threads);
         if constexpr (PIPE) {
             if (epi == EPI_BF16)
                 hipLaunchKernelGGL((gemm_i8_lds_kernel<TM, TN, BK, WM, WN, S, EPI_BF16>), grid, block, 0, s, kp);
@@ -853,14 +934,22 @@ struct TileEntry {
 #define W8A8_TILE(NAME, TM, TN, BK, WM, WN, GM, S)                                          \
     TileEntry {                                                                              \
         {NAME, TM, TN, BK, Tile<TM, TN, BK, WM, WN, S>::threads,                            \
-         Tile<TM, TN, BK, WM, WN, S>::lds},                                                  \
+         Tile<TM, TN, BK, WM, WN, S>::lds, 1, -1},                                           \
+            GM, &Tile<TM, TN, BK, WM, WN, S>::launch                                         \
+    }
+
+// The same pipelined tile with K divided among KSPLIT workgroups (BASE: its unsplit id).
+#define W8A8_TILE_SPLIT(NAME, TM, TN, BK, WM, WN, GM, S, KSPLIT, BASE)                    \
+    TileEntry {                                                                              \
+        {NAME, TM, TN, BK, Tile<TM, TN, BK, WM, WN, S>::threads,                            \
+         Tile<TM, TN, BK, WM, WN, S>::lds, KSPLIT, BASE},                                    \
             GM, &Tile<TM, TN, BK, WM, WN, S>::launch                                         \
     }
 
 #define W8A8_SKINNY(NAME, FMB, FNB, NW)                                                  \
     TileEntry {                                                                              \
         {NAME, 16 * FMB, 16 * FNB, 256, SkinnyTile<FMB, FNB, NW>::threads,                  \
-         SkinnyTile<FMB, FNB, NW>::lds},                                                     \
+         SkinnyTile<FMB, FNB, NW>::lds, 1, -1},                                              \
             1, &SkinnyTile<FMB, FNB, NW>::launch                                             \
     }
 
@@ -896,6 +985,16 @@ const TileEntry kTiles[] = {
     W8A8_TILE("m32n128k128w1x4s6", 32, 128, 128, 1, 4, 8, 6),
     W8A8_TILE("m64n64k128w2x2s8", 64, 64, 128, 2, 2, 8, 8),
     W8A8_TILE("m64n64k128w1x2s8", 64, 64, 128, 1, 2, 8, 8),
+    // Split-K: few output tiles and a long K; the int32 partials are summed by a second
+    // kernel that also runs the epilogue.
+    W8A8_TILE_SPLIT("m128n128k128w2x2s4_k2", 128, 128, 128, 2, 2, 8, 4, 2, 20),
+    W8A8_TILE_SPLIT("m128n128k128w2x2s4_k4", 128, 128, 128, 2, 2, 8, 4, 4, 20),
+    W8A8_TILE_SPLIT("m64n128k128w1x4s6_k2", 64, 128, 128, 1, 4, 8, 6, 2, 21),
+    W8A8_TILE_SPLIT("m64n128k128w1x4s6_k4", 64, 128, 128, 1, 4, 8, 6, 4, 21),
+    W8A8_TILE_SPLIT("m32n128k128w1x4s6_k4", 32, 128, 128, 1, 4, 8, 6, 4, 22),
+    W8A8_TILE_SPLIT("m128n256k128w2x2s3_k2", 128, 256, 128, 2, 2, 8, 3, 2, 3),
+    W8A8_TILE_SPLIT("m256n128k128w2x2s3_k2", 256, 128, 128, 2, 2, 8, 3, 2, 2),
+    W8A8_TILE_SPLIT("m160n256k128w1x4s3_k2", 160, 256, 128, 1, 4, 8, 3, 2, 7),
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -972,14 +1071,25 @@ int select_tile(int64_t M, int64_t N, int64_t K) {
     return fallback_tile(M, N, K);
 }
 
+// Splits of a split tile for K: panels of BK bytes dealt out in equal runs; a short K
+// gets fewer splits (one: no split at all).
+static int split_count(const TileInfo &t, int64_t K, int *chunk) {
+    const int64_t panels = (K + t.bk - 1) / t.bk;
+    const int64_t per = (panels + t.ksplit - 1) / t.ksplit;
+    if (chunk)
+        *chunk = (int)(per * t.bk);
+    return per > 0 ? (int)((panels + per - 1) / per) : 1;
+}
+
 size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K) {
-    (void)id; (void)M; (void)N; (void)K;
-    return 0;
+    if (id < 0 || id >= kNumTiles || kTiles[id].info.ksplit <= 1)
+        return 0;
+    const int splits = split_count(kTiles[id].info, K, nullptr);
+    return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
 }
 
 hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,
                        size_t ws_bytes, hipStream_t stream) {
-    (void)ws; (void)ws_bytes;
     const TileEntry &t = kTiles[id];
     const int tm = vec ? t.info.tm : GenericTile::tm;
     const int tn = vec ? t.info.tn : GenericTile::tn;
@@ -997,7 +1107,38 @@ hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *
     kp.out_vec = ov ? 1 : 0;
     if (ov && epi == EPI_BF16 && a.N % 8 == 0 && reinterpret_cast<uintptr_t>(a.out) % 16 == 0)
         kp.out_vec = 2;
-    return vec ? t.launch(epi, kp, stream) : GenericTile::launch(epi, kp, stream);
+    kp.k_split = 1;
+    kp.k_chunk = (int)a.K;
+    kp.part = nullptr;
+    kp.part_vec = 0;
+    if (!vec)
+        return GenericTile::launch(epi, kp, stream);
+    if (t.info.ksplit > 1) {
+        int chunk = 0;
+        const int splits = split_count(t.info, a.K, &chunk);
+        if (splits > 1) {
+            if (ws == nullptr || ws_bytes < tile_workspace_bytes(id, a.M, a.N, a.K))
+                return hipErrorInvalidValue;
+            kp.k_split = splits;
+            kp.k_chunk = chunk;
+            kp.part = static_cast<int32_t *>(ws);
+            kp.part_vec = (a.N % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0) ? 1 : 0;
+            // The tile kernel stores partials only, so its epilogue flavour is irrelevant.
+            const hipError_t e = t.launch(EPI_I32, kp, stream);
+            if (e != hipSuccess)
+                return e;
+            const int64_t items = kp.part_vec ? a.M * (a.N / 4) : a.M * a.N;
+            const unsigned blocks = (unsigned)((items + 255) / 256);
+            if (epi == EPI_BF16)
+                hipLaunchKernelGGL(splitk_reduce_kernel<EPI_BF16>, dim3(blocks), dim3(256), 0,
+                                   stream, kp);
+            else
+                hipLaunchKernelGGL(splitk_reduce_kernel<EPI_I32>, dim3(blocks), dim3(256), 0,
+                                   stream, kp);
+            return hipGetLastError();
+        }
+    }
+    return t.launch(epi, kp, stream);
 }
 
 }  // namespace w8a8

@@ -137,10 +137,15 @@ w8a8_status w8a8_smooth_factors(const float *x_amax, const float *w_amax, int64_
                                           as_stream(stream)));
 }
 
-size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    if (M <= 0 || N <= 0 || K < 0 || K > W8A8_MAX_K)
+size_t w8a8_gemm_workspace_bytes_ex(int64_t M, int64_t N, int64_t K, int tile_id) {
+    if (M <= 0 || N <= 0 || K < 0 || K > W8A8_MAX_K || tile_id < -1 ||
+        tile_id >= tile_count() || !product_ok(M, N))
         return 0;
-    return tile_workspace_bytes(select_tile(M, N, K), M, N, K);
+    return tile_workspace_bytes(tile_id >= 0 ? tile_id : select_tile(M, N, K), M, N, K);
+}
+
+size_t w8a8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    return w8a8_gemm_workspace_bytes_ex(M, N, K, -1);
 }
 
 w8a8_status w8a8_gemm_ex(const int8_t *xq, const float *x_scale, const int8_t *wq,
@@ -221,7 +226,10 @@ w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *ac
         return W8A8_ERR_ARG;
     if (M == 0 || N == 0)
         return W8A8_OK;
-    const int id = tile_id >= 0 ? tile_id : select_tile(M, N, K);
+    int id = tile_id >= 0 ? tile_id : select_tile(M, N, K);
+    // The debug accumulator has no workspace: a split tile runs unsplit.
+    if (tile_info(id)->base >= 0)
+        id = tile_info(id)->base;
     if (tile_workspace_bytes(id, M, N, K) > 0)
         return W8A8_ERR_ARG;
     return run_gemm(xq, nullptr, wq, nullptr, nullptr, acc, EPI_I32, M, N, K, nullptr, 0,

@@ -42,6 +42,8 @@ struct TileInfo {
     int tm, tn, bk;      // workgroup tile (tokens x channels x K step)
     int threads;         // workgroup size
     int lds_bytes;       // static LDS per workgroup
+    int ksplit;          // K divided among this many workgroups per tile (1: no split)
+    int base;            // for a split tile, the id of the same tile unsplit (else -1)
 };
 
 int tile_count();
@@ -50,7 +52,8 @@ const TileInfo *tile_info(int id);
 int select_tile(int64_t M, int64_t N, int64_t K);
 // The fallback rule alone (what a shape gets without a table entry).
 int default_tile(int64_t M, int64_t N, int64_t K);
-// Extra device scratch a tile needs for a shape (0 for the data-parallel tiles).
+// Extra device scratch a tile needs for a shape: the int32 partial products of a split
+// tile (splits x M x N x 4 bytes), 0 for the others.
 size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K);
 // Launch tile `id` with epilogue `epi`; `vec` selects the 16-byte-aligned load path.
 hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,

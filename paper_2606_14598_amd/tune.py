@@ -99,7 +99,8 @@ def sweep(iters: int, which: str = "all"):
     """Time every tile on every shape, on the shape's own synthetic inputs quantized by
     the library: the matrix cores' sustained rate depends on the operand bits
     (switching power), so uniform random or constant codes would mislead. The
-    weight-streaming tiles (made for M <= 128) are skipped above 128 tokens. The chip's
+    weight-streaming tiles (made for M <= 128) are skipped above 128 tokens, and the
+    split-K tiles where their unsplit tile already gives two workgroups per CU. The chip's
     power management needs ~15-20 ms of sustained load to settle after an idle gap (the
     input generation between shapes is one), so each shape first runs 30 ms of work,
     and every tile is timed twice, in two passes, keeping the faster."""
@@ -116,22 +117,34 @@ def sweep(iters: int, which: str = "all"):
         row = {"name": s.name, "M": s.M, "N": s.N, "K": s.K, "m_lo": lo, "m_hi": hi,
                "default": w8a8.tile_name(w8a8.default_tile(s.M, s.N, s.K)), "ms": {}}
         y = torch.empty((s.M, s.N), dtype=torch.bfloat16, device=dev)
+        nws = max(w8a8.gemm_workspace_bytes(s.M, s.N, s.K, t) for t in range(w8a8.tile_count()))
+        ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
         it = iters if s.ops < 5e14 else max(3, iters // 4)
-        cand = [t for t in range(w8a8.tile_count())
-                if not (s.M > 128 and w8a8.tile_name(t).startswith("skinny"))]
+        def wanted(t):
+            name = w8a8.tile_name(t)
+            if s.M > 128 and name.startswith("skinny"):
+                return False
+            d = _tile_dims(name)
+            # split-K only pays where the unsplit tiles leave CUs idle
+            if "_k" in name and -(-s.M // d[0]) * -(-s.N // d[1]) >= 2 * CUS:
+                return False
+            return True
+        cand = [t for t in range(w8a8.tile_count()) if wanted(t)]
         first = w8a8.select_tile(s.M, s.N, s.K)
-        time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=first, out=y), it, warm_ms=30.0)
+        time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=first, out=y, workspace=ws), it,
+                warm_ms=30.0)
         for _ in range(2):
             for t in cand:
                 name = w8a8.tile_name(t)
-                ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t, out=y), it)
+                ms = time_ms(lambda: w8a8.gemm(xq, sx, wq, sw, b, tile=t, out=y, workspace=ws),
+                             it)
                 row["ms"][name] = min(ms, row["ms"].get(name, ms))
         best = min(row["ms"], key=row["ms"].get)
         row["best"] = best
         row["best_tops"] = 2 * s.M * s.N * s.K / (row["ms"][best] * 1e-3) / 1e12
         print(json.dumps(row), flush=True)
         results.append(row)
-        del xq, sx, wq, sw, b, y
+        del xq, sx, wq, sw, b, y, ws
         torch.cuda.empty_cache()
     return results
 
@@ -152,7 +165,7 @@ def tile_rates(results, names):
             continue
         for n, ms in r["ms"].items():
             d = _tile_dims(n)
-            if d is None:
+            if d is None or "_k" in n:      # weight-streaming and split-K tiles: not modeled
                 continue
             tiles = -(-r["M"] // d[0]) * -(-r["N"] // d[1])
             waves = -(-tiles // CUS)

@@ -95,7 +95,7 @@ def _acc_case(M, N, K, seed):
     return xq_o, wq_o, oracle.gemm_acc(xq_o, wq_o)
 
 
-@pytest.mark.parametrize("tile", range(32))
+@pytest.mark.parametrize("tile", range(40))
 def test_acc_exact_every_tile(tile):
     """Every tile configuration gives the exact accumulator on ragged shapes (M, N not
     multiples of the tile, K tails, single rows/columns)."""
@@ -333,3 +333,31 @@ def test_graph_replays_match_eager(act, with_cm):
         # eager work between replays, through the same workspace
         w8a8.linear(xd[: M // 2], wq, sw, None, out=other[: M // 2], workspace=ws)
         torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- split-K tiles
+
+SPLIT_SHAPES = [(333, 512, 4096), (77, 520, 3136), (300, 391, 4112), (64, 256, 256),
+                (129, 384, 128)]
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+def test_split_k_tiles_exact(M, N, K):
+    """Every split-K tile through w8a8_gemm_ex: the int32 partials of the K-ranges are
+    summed in a second kernel, so the bf16 output equals the oracle's bit for bit
+    (several splits, a ragged last panel, K short enough for one or two splits, N not a
+    multiple of 4 for the scalar reduction)."""
+    x, w, b = si.make_inputs((M, K, N), seed=900 + K)
+    xq_o, sx_o = oracle.quantize_rows(x)
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o = oracle.epilogue(oracle.gemm_acc(xq_o, wq_o), sx_o, sw_o, b)
+    xq, sx = w8a8.quantize_act(dev_bf16(x))
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    bd = dev_bf16(b)
+    split_ids = [t for t in range(w8a8.tile_count()) if "_k" in w8a8.tile_name(t)]
+    assert split_ids
+    for t in split_ids:
+        y = host_bits(w8a8.gemm(xq, sx, wq, sw, bd, tile=t))
+        assert np.array_equal(y, y_o), w8a8.tile_name(t)
+        acc = host(w8a8.gemm_acc_i32(xq, wq, tile=t))   # runs unsplit
+        assert np.array_equal(acc, oracle.gemm_acc(xq_o, wq_o)), w8a8.tile_name(t)
