@@ -335,8 +335,12 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 256)
             return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        // K in (2048, 4096]: a wavefront per row, or the whole block per row when there
+        // are too few rows to fill the chip with one-wavefront rows (measured crossover
+        // near 4096 rows).
         if (nvec <= 512)
-            return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return rows < 4096 ? launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                               : launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 1024)
             return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 2048)

@@ -70,6 +70,19 @@ def test_quantizer_bytes_and_scales_exact(K):
                                                              s_o.view(np.uint32))
 
 
+@pytest.mark.parametrize("K", [2056, 3136, 4096])
+def test_quantizer_many_rows_exact(K):
+    """At 4096 rows and more, K in (2048, 4096] takes one wavefront per row (fewer rows
+    take the whole block per row): both variants against the oracle."""
+    x, _, _ = si.make_inputs((4200, K, 1), seed=700 + K, dist="student_t")
+    x[4099] = 0
+    q_o, s_o = oracle.quantize_rows(x)
+    q, s = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(q), q_o) and np.array_equal(host(s), s_o)
+    q2, s2 = w8a8.quantize_act(dev_bf16(x[:4095]))
+    assert np.array_equal(host(q2), q_o[:4095]) and np.array_equal(host(s2), s_o[:4095])
+
+
 def test_quantizer_unaligned_pointers():
     K = 256
     x, _, _ = si.make_inputs((20, K + 1, 1), seed=3)

@@ -97,7 +97,7 @@ def test_colmul_unaligned_multiplier_takes_the_element_path():
 # ---------------------------------------------------------------- GELU: within bound
 
 GELU_CASES = [(37, 8), (37, 264), (64, 4096), (9, 16384), (5, 20000), (11, 269),
-              (8300, 512)]
+              (8300, 512), (4100, 4096)]
 
 
 @pytest.mark.parametrize("M,K", GELU_CASES)
