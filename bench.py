@@ -129,7 +129,7 @@ def health_gate(dev) -> dict:
     tf = 2 * n ** 3 / (ms * 1e-3) / 1e12
     del a, b
     return {"bf16_gemm_8192_tflops": round(tf, 1), "threshold": HEALTH_MIN_BF16_TFLOPS,
-            "pass": tf >= HEALTH_MIN_BF16_TFLOPS}
+            "pass": tf >= HEALTH_MIN_BF16_TFLOPS, "smi": smi_snapshot()}
 
 
 def make_case(shape: dict, dev):
@@ -210,10 +210,49 @@ def cpu_baseline(shp, x, w, b, budget_s: float = 12.0) -> dict:
         total += time.perf_counter() - t0
         reps += 1
     ops = gemm_ops(rows, shp.N, shp.K) * reps
+    # single thread on the tiny workload (64 x 256 x 128), for scale
+    import synth_inputs as si
+    s0 = si.workload(0, "tiny")
+    x0, w0, b0 = si.make_inputs(s0)
+    wq0, sw0 = oracle.quantize_rows(w0, nthreads=1)
+    t0 = time.perf_counter()
+    n1 = 0
+    while time.perf_counter() - t0 < 0.5:
+        oracle.linear(x0, wq0, sw0, b0, nthreads=1)
+        n1 += 1
+    t1 = (time.perf_counter() - t0) / n1
+    oracle.quantize_rows(w0[:1], nthreads=threads)   # the thread setting is process-wide
     return {"value": round(ops / total / 1e12, 6), "unit": "TOPS", "cores": threads,
             "kind": "oracle",
             "sample": f"{reps} x {rows} of {shp.M} tokens of the {shp.M}x{shp.K}x{shp.N} "
-                      f"linear (quantize + int8 product + epilogue), {total:.1f} s"}
+                      f"linear (quantize + int8 product + epilogue), {total:.1f} s",
+            "cpu_model": cpu_model(),
+            "single_thread_tiny_ms": round(t1 * 1e3, 3)}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def smi_snapshot() -> dict:
+    """Clocks and temperature of GPU 0 as amd-smi reports them (read-only query, bounded
+    by a timeout); an error string if the tool is missing or fails."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--temperature",
+                            "--json"], capture_output=True, text=True, timeout=20)
+        if r.returncode != 0:
+            return {"error": (r.stderr or r.stdout).strip()[:200]}
+        data = json.loads(r.stdout)
+        return {"amd_smi": data if len(r.stdout) < 4000 else r.stdout[:4000]}
+    except Exception as e:  # noqa: BLE001 -- a snapshot must never fail the benchmark
+        return {"error": f"{type(e).__name__}: {e}"[:200]}
 
 
 # ------------------------------------------------------------------ main measurement
@@ -410,9 +449,16 @@ def all_shapes(args):
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
             ws = torch.empty(w8a8.linear_workspace_bytes(M, N, K), dtype=torch.uint8,
                              device=dev)
-            lin = graph_ms(lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws))
-            gem = graph_ms(lambda: w8a8.gemm(xq, sx, wq, sw, bd, out=y))
-            bf = graph_ms(lambda: F.linear(xd, wd, bd))
+            gws = torch.empty(max(1, w8a8.gemm_workspace_bytes(M, N, K)), dtype=torch.uint8,
+                              device=dev)
+            reps = {"lin": [], "gem": [], "bf": []}
+            for _ in range(5):
+                reps["lin"].append(graph_ms(lambda: w8a8.linear(xd, wq, sw, bd, out=y,
+                                                                workspace=ws)))
+                reps["gem"].append(graph_ms(lambda: w8a8.gemm(xq, sx, wq, sw, bd, out=y,
+                                                              workspace=gws)))
+                reps["bf"].append(graph_ms(lambda: F.linear(xd, wd, bd)))
+            lin, gem, bf = (sorted(reps[k])[2] for k in ("lin", "gem", "bf"))
             ops = gemm_ops(M, N, K)
             gb = gemm_bytes(M, N, K)
             rec = {"config": cfg, "shape": shp.name, "M": M, "K": K, "N": N,
@@ -425,9 +471,32 @@ def all_shapes(args):
                    "gemm_hbm_GB_s": round(gb / gem / 1e6, 1),
                    "gemm_pct_hbm": round(100 * gb / gem / 1e6 / PEAK_HBM_GBS, 2),
                    "bound": "mfma" if ops / gb > PEAK_INT8_TOPS * 1e3 / PEAK_HBM_GBS else "hbm",
-                   "speedup_linear_vs_bf16": round(bf / lin, 3)}
+                   "speedup_linear_vs_bf16": round(bf / lin, 3),
+                   "timing": "median of 5 repeats"}
+            if M <= 333:
+                # cold: a 512 MB scrub write before every call, so the 256 MB MALL cannot
+                # serve the weight; each call timed alone with HIP events
+                scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+                cold = {"lin": [], "gem": [], "bf": []}
+                fns = {"lin": lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws),
+                       "gem": lambda: w8a8.gemm(xq, sx, wq, sw, bd, out=y, workspace=gws),
+                       "bf": lambda: F.linear(xd, wd, bd)}
+                for _ in range(10):
+                    for k, f in fns.items():
+                        scrub.fill_(1)
+                        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        st.record()
+                        f()
+                        en.record()
+                        torch.cuda.synchronize()
+                        cold[k].append(st.elapsed_time(en))
+                cl, cg, cb = (sorted(cold[k])[5] for k in ("lin", "gem", "bf"))
+                rec["cold_us"] = {"linear": round(cl * 1e3, 2), "gemm": round(cg * 1e3, 2),
+                                  "bf16_linear": round(cb * 1e3, 2)}
+                rec["cold_gemm_hbm_GB_s"] = round(gb / cg / 1e6, 1)
+                del scrub
             print(json.dumps(rec), flush=True)
-            del xd, wd, bd, wq, sw, xq, sx, y, ws
+            del xd, wd, bd, wq, sw, xq, sx, y, ws, gws
 
 
 def recipe(args):
