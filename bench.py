@@ -240,6 +240,58 @@ def cpu_model() -> str:
     return "unknown"
 
 
+def gfx_clock_mhz(data) -> list:
+    """Current gfx clocks (MHz) found in an amd-smi metric --clock JSON document."""
+    out = []
+    def walk(o, key=""):
+        if isinstance(o, dict):
+            if key.startswith("gfx") and isinstance(o.get("clk"), dict):
+                v = o["clk"].get("value")
+                if isinstance(v, (int, float)):
+                    out.append(float(v))
+            for k, v in o.items():
+                walk(v, str(k))
+        elif isinstance(o, list):
+            for v in o:
+                walk(v, key)
+    walk(data)
+    return out
+
+
+def clock_under_load(fn, seconds: float = 3.0) -> dict:
+    """The gfx clock while fn runs back to back: amd-smi is polled from a host thread
+    while the GPU stays busy; the mean over polls and engines is reported."""
+    import subprocess
+    import threading
+    import torch
+    samples, errors = [], []
+
+    def poll():
+        for _ in range(3):
+            try:
+                r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--json"],
+                                   capture_output=True, text=True, timeout=20)
+                if r.returncode == 0:
+                    samples.extend(gfx_clock_mhz(json.loads(r.stdout)))
+                else:
+                    errors.append((r.stderr or r.stdout).strip()[:120])
+            except Exception as e:  # noqa: BLE001 -- a measurement aid, never fatal
+                errors.append(f"{type(e).__name__}: {e}"[:120])
+    th = threading.Thread(target=poll)
+    t0 = time.perf_counter()
+    th.start()
+    while th.is_alive() and time.perf_counter() - t0 < 60:
+        for _ in range(200):
+            fn()
+        torch.cuda.synchronize()
+    th.join(timeout=60)
+    if not samples:
+        return {"error": errors[0] if errors else "no gfx clock in amd-smi output"}
+    return {"gfx_mhz_mean": round(sum(samples) / len(samples), 1),
+            "gfx_mhz_min": min(samples), "gfx_mhz_max": max(samples),
+            "samples": len(samples), "source": "amd-smi metric --clock (reported gfx clock)"}
+
+
 def smi_snapshot() -> dict:
     """Clocks and temperature of GPU 0 as amd-smi reports them (read-only query, bounded
     by a timeout); an error string if the tool is missing or fails."""
@@ -371,6 +423,12 @@ def run(args) -> dict:
         comp["weight_quant_ms"] = round(time_weight_quant(wd), 4)
         rec["comparators"] = comp
         rec["vs_bf16_gemm"] = comp["speedup_vs_bf16"]
+        # the clock the chip holds under this GEMM, and the peak at that clock
+        clk = clock_under_load(gemm)
+        rec["roofline"]["clock_under_load"] = clk
+        if "gfx_mhz_mean" in clk:
+            rec["roofline"]["pct_of_peak_at_measured_clock"] = round(
+                100 * gemm_tops / (PEAK_INT8_TOPS * clk["gfx_mhz_mean"] / 2400.0), 2)
         shapes = []
         del xd, wd, xq, y
         shp2, x2, w2, b2, xd2, wd2, bd2, wq2, sw2 = make_case(VARIANT, dev)
