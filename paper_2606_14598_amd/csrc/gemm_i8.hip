@@ -4,22 +4,28 @@
 // Y[m][n] = bf16(fmaf((float)acc[m][n], sx[m] * sw[n], b[n])),
 // acc[m][n] = sum_k Xq[m][k] * Wq[n][k], with Xq [M,K] and Wq [N,K] both K-contiguous.
 //
-// Design (one workgroup per TM x TN output tile):
-//   * v_mfma_i32_32x32x32_i8: the weight tile is the matrix-core A operand (its 32 rows
-//     are output channels n) and the activation tile the B operand (its 32 columns are
-//     tokens m). The accumulator layout then gives each lane 4 consecutive channels of
-//     one token, so the bf16 epilogue writes 8 contiguous bytes per lane-group and the
-//     per-channel scale/bias come in as 16/8-byte vectors.
-//   * K-panels of BK bytes are staged in LDS, double buffered: the global loads of
-//     panel k+1 (buffer loads: rows past M/N and bytes past K read as zero, so ragged
-//     tiles need no branches) are in flight while the matrix cores work on panel k.
-//   * LDS rows are BK bytes; their 16-byte chunks are XOR-swizzled by row so that both
-//     the 16-byte stores of a wavefront and the 16-byte operand reads (32 rows x one
-//     chunk per half-wavefront) hit distinct bank groups.
-//   * Workgroup ids are remapped so that each XCD (which receives every 8th id) owns a
-//     contiguous run of tiles, traversed in groups of GM token-tiles, so the operand
-//     panels a run touches stay in that XCD's L2.
-//   * The integer accumulation is exact, so every tiling gives identical bits.
+// Kernels (one workgroup per TM x TN output tile unless noted):
+//   * gemm_i8_lds_kernel, the main one. v_mfma_i32_32x32x32_i8 with the weight tile as
+//     operand A (rows = output channels) and the activation tile as operand B (columns
+//     = tokens), so each lane's accumulator holds 4 consecutive channels of one token.
+//     K-panels of BK bytes move global -> LDS by direct-to-LDS buffer loads into an
+//     S-stage ring (panel k+S-1 requested while panel k is multiplied); rows past M/N
+//     and bytes past K read as zero through the buffer descriptors, so ragged tiles
+//     need no branches. LDS rows are XOR-swizzled by row, conflict-free for the DMA
+//     writes and the fragment reads. The bf16 epilogue stages 32-token chunks in LDS and
+//     writes whole 16-byte row segments with streaming stores.
+//   * Split-K variants of it: K divided among several workgroups per tile, int32
+//     partials in a workspace, summed (exactly) by splitk_reduce_kernel, which also runs
+//     the epilogue.
+//   * gemm_i8_kernel: register-staged copies, for small tiles and for operands that are
+//     not 16-byte aligned or whose K is not a multiple of 16 (byte loads).
+//   * gemm_i8_skinny_kernel: few tokens (M <= 128). A workgroup streams 16*FNB weight
+//     rows once for all tokens with v_mfma_i32_16x16x64_i8, its wavefronts splitting K,
+//     partial sums reduced in LDS.
+// Workgroup ids are remapped so that each XCD (which receives every 8th id) owns a
+// contiguous run of tiles, traversed in groups of GM token-tiles: the operand panels a
+// run touches stay in that XCD's L2. The integer accumulation is exact, so every tile,
+// split and order gives identical bits.
 #include "w8a8_internal.hpp"
 
 #include <utility>
@@ -369,16 +375,20 @@ __device__ __forceinline__ void barrier_nofence() {
 }
 
 // Pipelined variant for 16-byte aligned operands with K % 16 == 0.
-//   * Panels go straight from global memory to LDS (buffer_load_dwordx4 ... lds): lane l
-//     of the i-th load of wavefront w fills LDS chunk c = i*NT + 64w + l, i.e. row
-//     c / CPR, physical chunk c % CPR, and therefore fetches logical chunk
-//     (c % CPR) ^ swz(row) of that row. No staging registers, no ds_write.
+//   * Panels go straight from global memory to LDS (buffer_load_dwordx4 ... lds). Load
+//     g of a panel (wavefront g % NW issues it) fills 64 chunks of 16 bytes of the
+//     weight part (g < IW) or of the activation part: lane l writes chunk 64g' + l, i.e.
+//     row RPI*g' + l/CPR, physical chunk l % CPR, and therefore fetches logical chunk
+//     (l % CPR) ^ swz(row) of that row. No staging registers, no ds_write.
 //   * S LDS stages in a ring: panel k+S-1 is requested while panel k is multiplied, so a
 //     load has S-1 panels of MFMA work to arrive; one wait + barrier per panel makes
-//     panel k+1 visible to every wavefront.
+//     panel k+1 visible to every wavefront (with S >= 3 one K-step before panel k ends,
+//     so the next panel's first fragments are read behind the last K-step's MFMAs).
 //   * MFMA operand fragments are double-buffered across the BK/32 K-steps of a panel:
-//     each K-step is two fenced groups, (1) the ds_reads of the next K-step's fragments
-//     and a slice of the loads of panel k+S-1, (2) this K-step's MFMAs back to back.
+//     each K-step issues the ds_reads of the next K-step's fragments and its share of
+//     the loads of panel k+S-1, one memory instruction between consecutive MFMAs.
+//   * Split-K (kp.k_split > 1): the workgroup covers one K-range of its tile and stores
+//     the int32 partial instead of running the epilogue.
 template <int TM, int TN, int BK, int WM, int WN, int S, int EPI>
 __global__ void __launch_bounds__(WM *WN * 64)
 gemm_i8_lds_kernel(KParams kp) {
