@@ -75,11 +75,21 @@ def quant_bytes(M: int, K: int) -> int:
     return 3 * M * K + 4 * M
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and blank space, so that a comment edit does not
+    count as a kernel change (string literals here hold no comment markers)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def gemm_source_hash() -> str:
+    """Identity of the GEMM kernel code (comments and whitespace ignored): the stored
+    HBM-traffic counters apply only while it is unchanged."""
     h = hashlib.sha256()
     for p in GEMM_SRC:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 
