@@ -1014,28 +1014,31 @@ struct TableEntry {
     int64_t m_lo, m_hi, n, k;
     int tile;
 };
+struct TileCost {
+    double c;   // ms per round, fixed part
+    double d;   // ms per round per 1e9 (K * TM * TN)
+};
 #include "tile_table.inc"
 
-static_assert(sizeof(kTileRate) / sizeof(kTileRate[0]) == kNumTiles, "one rate per tile");
+static_assert(sizeof(kTileCost) / sizeof(kTileCost[0]) == kNumTiles, "one cost per tile");
 
 // Shapes without a table entry. Above 128 tokens a wave-quantization cost model picks
-// the tile: a launch of T workgroups on 256 CUs takes ceil(T / 256) rounds, each as long
-// as one tile's work (TM x TN x K) at the tile's sustained rate (kTileRate, measured
-// offline); K is common to every candidate and drops out. With few tokens the
-// weight-streaming kernels take over.
+// the tile: a launch of T workgroups on 256 CUs takes ceil(T / 256) rounds, and a round
+// of tile t costs c_t + d_t * K * TM * TN / 1e9 (kTileCost, fitted offline to the
+// sweep). With few tokens the weight-streaming kernels take over.
 int fallback_tile(int64_t M, int64_t N, int64_t K) {
-    (void)K;
     const int64_t cus = 256;
     if (M > 128) {
         int best = -1;
         double best_cost = 0.0;
         for (int id = 0; id < kNumTiles; ++id) {
-            if (!(kTileRate[id] > 0.0f))
+            if (!(kTileCost[id].d > 0.0))
                 continue;
             const TileInfo &t = kTiles[id].info;
             const int64_t tiles = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
             const int64_t rounds = (tiles + cus - 1) / cus;
-            const double cost = (double)rounds * t.tm * t.tn / kTileRate[id];
+            const double cost =
+                (double)rounds * (kTileCost[id].c + kTileCost[id].d * (double)K * t.tm * t.tn * 1e-9);
             if (best < 0 || cost < best_cost) {
                 best = id;
                 best_cost = cost;

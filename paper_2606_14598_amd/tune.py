@@ -34,7 +34,7 @@ import synth_inputs as si  # noqa: E402
 HEADER = """// Offline-chosen GEMM tile per shape: {M lower bound, M upper bound, N, K, tile id}.
 // Written by paper_2606_14598_amd/tune.py from a timed sweep of every tile on MI355X;
 // shapes not listed use the fallback rule in gemm_i8.hip, whose cost model takes each
-// tile's sustained rate from kTileRate below.
+// tile's per-round cost from kTileCost below.
 """
 
 CUS = 256
@@ -154,32 +154,46 @@ def _tile_dims(name):
     return tuple(int(g) for g in m.groups()) if m else None
 
 
-def tile_rates(results, names):
-    """Sustained TOP/s of each LDS-staged tile: the median over swept shapes with at least
-    512 tokens of its achieved rate divided by its wave efficiency (tiles / (waves *
-    CUs)), i.e. what it would reach with every CU busy. 0 for the weight-streaming tiles
-    (not modeled)."""
-    per = {n: [] for n in names}
-    for r in results:
-        if r["M"] < 512:
+def tile_costs(results, names):
+    """Per-round cost model of each LDS-staged tile, fitted to the sweep: a launch of T
+    workgroups takes ceil(T / CUS) rounds, each costing c + d * (K * TM * TN / 1e9) ms
+    (c: the fixed part of a round -- launch share, prologue, epilogue; d: the
+    per-multiply-accumulate part). Least squares on relative error over the swept shapes
+    with more than 128 tokens; c is held at 0 if it fits negative. (0, 0) for the
+    weight-streaming and split-K tiles (not modeled)."""
+    out = []
+    for n in names:
+        d = _tile_dims(n)
+        rows, ys = [], []
+        if d is not None and "_k" not in n:
+            for r in results:
+                if r["M"] <= 128 or n not in r["ms"]:
+                    continue
+                tiles = -(-r["M"] // d[0]) * -(-r["N"] // d[1])
+                rounds = -(-tiles // CUS)
+                rows.append([rounds, rounds * r["K"] * d[0] * d[1] / 1e9])
+                ys.append(r["ms"][n])
+        if len(rows) < 2:
+            out.append((0.0, 0.0))
             continue
-        for n, ms in r["ms"].items():
-            d = _tile_dims(n)
-            if d is None or "_k" in n:      # weight-streaming and split-K tiles: not modeled
-                continue
-            tiles = -(-r["M"] // d[0]) * -(-r["N"] // d[1])
-            waves = -(-tiles // CUS)
-            per[n].append(2 * r["M"] * r["N"] * r["K"] / (ms * 1e-3) / 1e12
-                          / (tiles / (waves * CUS)))
-    return [float(np.median(per[n])) if per[n] else 0.0 for n in names]
+        A = np.array(rows)
+        y = np.array(ys)
+        w = 1.0 / y
+        c, dd = np.linalg.lstsq(A * w[:, None], y * w, rcond=None)[0]
+        if c < 0:
+            c = 0.0
+            dd = float(np.sum(A[:, 1] * w * w * y) / np.sum((A[:, 1] * w) ** 2))
+        out.append((float(c), float(dd)) if dd > 0 else (0.0, 0.0))
+    return out
 
 
 def write_table(results, path):
     names = [w8a8.tile_name(t) for t in range(w8a8.tile_count())]
-    rates = tile_rates(results, names)
-    lines = [HEADER, "static const float kTileRate[] = {"]
-    for n, v in zip(names, rates):
-        lines.append(f"    {v:.0f}.0f,  // {n}")
+    costs = tile_costs(results, names)
+    lines = [HEADER, "// Fallback cost model per tile: {c, d}, one round = c + d * K * TM * TN / 1e9 ms.",
+             "static const TileCost kTileCost[] = {"]
+    for n, (c, dd) in zip(names, costs):
+        lines.append(f"    {{{c:.6e}, {dd:.6e}}},  // {n}")
     lines.append("};")
     lines.append("")
     lines.append("static const TableEntry kTileTable[] = {")

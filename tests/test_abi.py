@@ -161,34 +161,35 @@ def test_python_binding_checks_transform_arguments():
         w8a8.col_absmax(x, accumulate=True)
 
 
-def _table_rates():
+def _table_costs():
     path = os.path.join(ROOT, "paper_2606_14598_amd", "csrc", "tile_table.inc")
     text = open(path).read()
-    body = text[text.index("kTileRate[] = {"):]
+    body = text[text.index("kTileCost[] = {"):]
     body = body[:body.index("};")]
-    return [float(v) for v in re.findall(r"([0-9.]+)f,", body)]
+    return [(float(c), float(d)) for c, d in re.findall(r"\{([-0-9.e+]+), ([-0-9.e+]+)\}", body)]
 
 
 def test_default_tile_follows_the_wave_cost_model(lib):
-    rates = _table_rates()
+    costs = _table_costs()
     n = lib.w8a8_tile_count()
-    assert len(rates) == n
+    assert len(costs) == n
     dims = []
     for i in range(n):
         m = re.match(r"m(\d+)n(\d+)", lib.w8a8_tile_name(i).decode())
         dims.append((int(m.group(1)), int(m.group(2))) if m else None)
     for M, N, K in [(129, 4096, 4096), (333, 16384, 4096), (512, 4608, 4608),
                     (2560, 4096, 4096), (4110, 13824, 4608), (5000, 7000, 4096),
-                    (16384, 4608, 53248)]:
+                    (16384, 4608, 53248), (300, 5000, 2048)]:
         best, cost = None, None
         for i in range(n):
-            if rates[i] <= 0:
+            c, d = costs[i]
+            if d <= 0:
                 continue
             tm, tn = dims[i]
             rounds = -(-(-(-M // tm) * -(-N // tn)) // 256)
-            c = rounds * tm * tn / rates[i]
-            if cost is None or c < cost:
-                best, cost = i, c
+            est = rounds * (c + d * K * tm * tn * 1e-9)
+            if cost is None or est < cost:
+                best, cost = i, est
         assert lib.w8a8_default_tile(M, N, K) == best, (M, N, K)
     # few tokens: weight-streaming tiles
     for M in (1, 16, 64, 128):
