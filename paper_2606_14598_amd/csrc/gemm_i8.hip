@@ -190,7 +190,17 @@ __device__ __forceinline__ void store_tile(const i32x16 (&acc)[FN][FM], const KP
 // indexed from the wavefront's first token / channel; out-of-range entries are 0).
 // Needs a barrier before it (the region overlaps the panel stages) and
 // 32 * (2*WTN + 16) bytes of LDS per wavefront.
-template <int FN, int FM>
+//
+// With one wavefront per SIMD (NW <= 4) nothing else hides the LDS latencies, so the
+// chunks are software-pipelined: the row reads of chunk j are issued, then chunk j+1 is
+// converted into the same region while they are in flight, then chunk j is stored. One
+// region suffices because a wavefront's LDS instructions execute in order: the reads of
+// chunk j see its data before the writes of chunk j+1 replace it. The channel scales and
+// bias of narrow wavefront tiles (FN <= 2) are then held in registers. With more
+// wavefronts per SIMD registers are short and the other wavefronts hide the latencies:
+// each chunk is converted, read back and stored in turn, with the vectors read from LDS.
+// A tile that lies wholly inside the output stores without bounds tests.
+template <int FN, int FM, int NW>
 __device__ __forceinline__ void store_tile_bf16_lds(const i32x16 (&acc)[FN][FM],
                                                     const KParams &kp, int64_t m_base,
                                                     int64_t n_base, int lane,
@@ -199,26 +209,54 @@ __device__ __forceinline__ void store_tile_bf16_lds(const i32x16 (&acc)[FN][FM],
     constexpr int WTN = FN * 32;
     constexpr int RS = 2 * WTN + 16;          // region row stride in bytes
     constexpr int CPRO = WTN / 8;             // 16-byte chunks per output row
+    constexpr int RPQ = 64 / CPRO;            // rows covered by one 64-lane read
+    constexpr int NQ = 32 / RPQ;              // reads (and stores) per lane per chunk
+    static_assert(64 % CPRO == 0 && 32 % RPQ == 0, "row split");
     const GemmArgs &a = kp.a;
     const int64_t M = a.M, N = a.N;
     const int h = lane >> 5, r = lane & 31;
     uint16_t *out = static_cast<uint16_t *>(a.out);
+
+    constexpr bool PIPE = NW <= 4;
+    constexpr bool HOIST = PIPE && FN <= 2;
+    constexpr int HF = HOIST ? FN : 1;
+    f32x4 sw4[HF][4], b4[HF][4];
+    if constexpr (HOIST) {
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
-        const float sxm = t_sx[j * 32 + r];
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int c = i * 32 + g * 8 + h * 4;
+                sw4[i][g] = *reinterpret_cast<const f32x4 *>(t_sw + c);
+                b4[i][g] = *reinterpret_cast<const f32x4 *>(t_b + c);
+            }
+    }
+    float sxv[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+        sxv[j] = t_sx[j * 32 + r];
+    // Chunk j into the region: this lane's token r, channels c .. c+3 per (i, g).
+    auto convert = [&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        const float sxm = sxv[j];
 #pragma unroll
         for (int i = 0; i < FN; ++i) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                // This lane's channels: c .. c+3 of the wavefront's tile.
                 const int c = i * 32 + g * 8 + h * 4;
-                const f32x4 sw4 = *reinterpret_cast<const f32x4 *>(t_sw + c);
-                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(t_b + c);
+                f32x4 s4, c4;
+                if constexpr (HOIST) {
+                    s4 = sw4[i][g];
+                    c4 = b4[i][g];
+                } else {
+                    s4 = *reinterpret_cast<const f32x4 *>(t_sw + c);
+                    c4 = *reinterpret_cast<const f32x4 *>(t_b + c);
+                }
                 uint16_t hv[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float sc = sxm * sw4[e];
-                    const float y = __builtin_fmaf((float)acc[i][j][4 * g + e], sc, b4[e]);
+                    const float sc = sxm * s4[e];
+                    const float y = __builtin_fmaf((float)acc[i][j][4 * g + e], sc, c4[e]);
                     hv[e] = __builtin_bit_cast(uint16_t, (__bf16)y);
                 }
                 uint2 pk;
@@ -227,22 +265,40 @@ __device__ __forceinline__ void store_tile_bf16_lds(const i32x16 (&acc)[FN][FM],
                 *reinterpret_cast<uint2 *>(region + r * RS + c * 2) = pk;
             }
         }
-        // Read back whole rows: lane-chunk q covers row q / CPRO, 8 channels at q % CPRO.
+    };
+    // Lane's share of a chunk: rows row0 + RPQ*s, 8 channels at chunk ch.
+    const int row0 = lane / CPRO, ch = lane % CPRO;
+    const bool full = (m_base + FM * 32 <= M) && (n_base + WTN <= N);   // wave-uniform
+    if constexpr (PIPE)
+        convert(std::integral_constant<int, 0>{});
+    [&]<int... j>(std::integer_sequence<int, j...>) {
+        ([&] {
+            if constexpr (!PIPE)
+                convert(std::integral_constant<int, j>{});
+            u32x4 v[NQ];
 #pragma unroll
-        for (int q0 = 0; q0 < 32 * CPRO; q0 += 64) {
-            const int q = q0 + lane;
-            const int row = q / CPRO, ch = q % CPRO;
-            const uint4 v = *reinterpret_cast<const uint4 *>(region + row * RS + ch * 16);
-            const int64_t mm = m_base + j * 32 + row;
+            for (int s = 0; s < NQ; ++s)
+                v[s] = *reinterpret_cast<const u32x4 *>(region + (row0 + RPQ * s) * RS + ch * 16);
+            if constexpr (PIPE && j + 1 < FM)
+                convert(std::integral_constant<int, j + 1>{});
+            const int64_t mm = m_base + j * 32 + row0;
             const int64_t nn = n_base + ch * 8;
             // Streaming (nontemporal) stores: the output is not read again by this
             // kernel, and lines that bypass the L2's write-back set leave less to flush
             // when the kernel ends.
-            if (mm < M && nn < N)
-                __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w},
-                                            reinterpret_cast<u32x4 *>(out + mm * N + nn));
-        }
-    }
+            u32x4 *dst = reinterpret_cast<u32x4 *>(out + mm * N + nn);
+            if (full) {
+#pragma unroll
+                for (int s = 0; s < NQ; ++s)
+                    __builtin_nontemporal_store(v[s], dst + (int64_t)s * RPQ * N / 8);
+            } else {
+#pragma unroll
+                for (int s = 0; s < NQ; ++s)
+                    if (mm + RPQ * s < M && nn < N)
+                        __builtin_nontemporal_store(v[s], dst + (int64_t)s * RPQ * N / 8);
+            }
+        }(), ...);
+    }(std::make_integer_sequence<int, FM>{});
 }
 
 template <int TM, int TN, int BK, int WM, int WN, bool VEC, int EPI>
@@ -689,7 +745,7 @@ gemm_i8_lds_kernel(KParams kp) {
         static_assert(NW * 32 * (2 * WTN + 16) <= S * STAGE, "epilogue staging");
         if (kp.out_vec == 2) {
             barrier_nofence();   // every wavefront is done reading the panel stages
-            store_tile_bf16_lds<FN, FM>(acc, kp, m0 + wm * WTM, n0 + wn * WTN, lane,
+            store_tile_bf16_lds<FN, FM, NW>(acc, kp, m0 + wm * WTM, n0 + wn * WTN, lane,
                                         smem + wave * 32 * (2 * WTN + 16), t_sx + wm * WTM,
                                         t_sw + wn * WTN, t_b + wn * WTN);
             return;

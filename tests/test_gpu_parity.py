@@ -163,7 +163,7 @@ def test_acc_against_torch_int_mm():
 
 LINEAR_SMALL = [(64, 256, 128, "outlier"), (257, 384, 391, "student_t"),
                 (130, 3136, 260, "gelu"), (1, 4096, 130, "outlier"), (77, 264, 64, "outlier"),
-                (45, 269, 77, "student_t")]
+                (45, 269, 77, "student_t"), (300, 512, 200, "outlier")]
 
 
 @pytest.mark.parametrize("M,K,N,dist", LINEAR_SMALL)
