@@ -71,6 +71,13 @@ __device__ __forceinline__ uint2 code8(uint4 d, float inv) {
     return o;
 }
 
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+// Swap with the neighbouring lane (lane l <-> l ^ 1) by a DPP quad permutation [1,0,3,2].
+__device__ __forceinline__ uint32_t swap_lane_pair(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+}
+
 struct RowScale {
     float inv;    // 127 / a, or 0 for a zero row
     float scale;  // a / 127, or 0 for a zero row
@@ -157,6 +164,7 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
     const int sub = threadIdx.x / TPR;
     const int64_t nvec = K >> 3;
     const int64_t groups = (rows + RPB - 1) / RPB;
+    const bool wide = (K % 16 == 0) && (reinterpret_cast<uintptr_t>(q) % 16 == 0);
     __shared__ uint32_t part[RPB][TPR / 64];
 
     float cmr[CM ? NV : 1][8];
@@ -221,22 +229,49 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
         if (t == 0)
             scale[row] = rs.scale;
         uint2 *dst = reinterpret_cast<uint2 *>(q + row * K);
+        uint2 cv[NV];
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-            const int64_t vi = (int64_t)j * TPR + t;
-            if (vi < nvec) {
-                if constexpr (PLAIN) {
-                    dst[vi] = code8(d[j], rs.inv);
-                } else {
-                    uint32_t c[8];
+            if constexpr (PLAIN) {
+                cv[j] = code8(d[j], rs.inv);
+            } else {
+                uint32_t c[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        c[e] = code_f(f[j][e], rs.inv);
-                    uint2 o;
-                    o.x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-                    o.y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
-                    dst[vi] = o;
-                }
+                for (int e = 0; e < 8; ++e)
+                    c[e] = code_f(f[j][e], rs.inv);
+                cv[j].x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+                cv[j].y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
+            }
+        }
+        if (NV % 2 == 0 && wide) {
+            // 16-byte streaming stores (K % 16 == 0, q 16-byte aligned). Vectors j and
+            // j+1 of lane t are j*TPR + t and (j+1)*TPR + t; neighbouring lanes swap one
+            // code word pair so that the even lane holds vectors j*TPR + t, +1 and the
+            // odd lane (j+1)*TPR + t - 1, +1. Streaming 16-byte stores leave no dirty
+            // lines in this XCD's L2 for the kernel's end to write back before the
+            // consumer starts (plain stores, and 8-byte streaming ones, delayed the next
+            // kernel by 1.5-2.5 us).
+            const bool odd = t & 1;
+#pragma unroll
+            for (int j = 0; j + 1 < NV; j += 2) {
+                // Selects on scalars (a select between array elements would put the
+                // array in memory).
+                const uint32_t a0 = cv[j].x, a1 = cv[j].y, b0 = cv[j + 1].x, b1 = cv[j + 1].y;
+                const uint32_t r0 = swap_lane_pair(odd ? a0 : b0);
+                const uint32_t r1 = swap_lane_pair(odd ? a1 : b1);
+                const int64_t v0 = (int64_t)(odd ? j + 1 : j) * TPR + t - (odd ? 1 : 0);
+                const u32x4v o = odd ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
+                if (v0 + 1 < nvec)
+                    __builtin_nontemporal_store(o, reinterpret_cast<u32x4v *>(dst + v0));
+                else if (v0 < nvec)
+                    dst[v0] = make_uint2(o.x, o.y);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NV; ++j) {
+                const int64_t vi = (int64_t)j * TPR + t;
+                if (vi < nvec)
+                    dst[vi] = cv[j];
             }
         }
     };
