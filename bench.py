@@ -12,7 +12,10 @@ Prints one JSON line. Besides the required fields it carries:
   roofline      the GEMM kernel's achieved int8 ops/s (2MNK per launch / its mean
                 HIP-event duration inside the timed region) against MI355X's dense int8
                 peak; traffic = HBM bytes per launch from rocprofv3 counters when they
-                were taken on the current kernel source, else null
+                were taken on the current kernel source, else null; mfma_ceiling =
+                what the int8 matrix cores sustain on this workload's own codes (the
+                GEMM's MFMA sequence replayed from registers), against which the GEMM's
+                rate is also given
   cpu_baseline  the CPU oracle timed on this host over a bounded row sample
   shapes        per-shape figures for the workload's QKV variant (N = 12288) and the
                 linear as a whole, with bf16 / fake-quant / unfused-int8 comparators
@@ -302,6 +305,31 @@ def clock_under_load(fn, seconds: float = 3.0) -> dict:
             "samples": len(samples), "source": "amd-smi metric --clock (reported gfx clock)"}
 
 
+def mfma_ceiling(w8a8, xq, wq, gemm_tops: float, iters: int = 800, warm_ms: float = 30.0,
+                 n: int = 10) -> dict:
+    """The int8 matrix-core ceiling on this workload's own codes: the GEMM's per-K-step
+    MFMA sequence replayed from registers (w8a8_mfma_ceiling), warmed by time, then n
+    launches between HIP events."""
+    import time
+    import torch
+    sums = torch.empty(1024, dtype=torch.int32, device=xq.device)
+
+    def f():
+        w8a8.mfma_ceiling(xq, wq, iters, out=sums)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < warm_ms:
+        f()
+        torch.cuda.synchronize()
+    ms = time_loop(f, n, warmup=0)
+    tops = w8a8.mfma_ceiling_ops(iters) / (ms * 1e-3) / 1e12
+    return {"tops": round(tops, 1), "frac_of_peak": round(tops / PEAK_INT8_TOPS, 4),
+            "gemm_frac_of_ceiling": round(gemm_tops / tops, 4),
+            "what": "the GEMM's MFMA sequence (per wavefront and K-step, 2 weight x 5 token "
+                    "fragments of v_mfma_i32_32x32x32_i8) replayed from registers on this "
+                    "workload's Xq/Wq fragments, no memory traffic (w8a8_mfma_ceiling)"}
+
+
 def smi_snapshot() -> dict:
     """Clocks and temperature of GPU 0 as amd-smi reports them (read-only query, bounded
     by a timeout); an error string if the tool is missing or fails."""
@@ -439,6 +467,8 @@ def run(args) -> dict:
         if "gfx_mhz_mean" in clk:
             rec["roofline"]["pct_of_peak_at_measured_clock"] = round(
                 100 * gemm_tops / (PEAK_INT8_TOPS * clk["gfx_mhz_mean"] / 2400.0), 2)
+        # what the matrix cores sustain on these very codes
+        rec["roofline"]["mfma_ceiling"] = mfma_ceiling(w8a8, xq, wq, gemm_tops)
         shapes = []
         del xd, wd, xq, y
         shp2, x2, w2, b2, xd2, wd2, bd2, wq2, sw2 = make_case(VARIANT, dev)

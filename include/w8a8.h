@@ -191,6 +191,25 @@ w8a8_status w8a8_smooth_factors(const float *x_amax, const float *w_amax, int64_
                                 float alpha, float *smooth, float *smooth_inv,
                                 void *stream);
 
+/* ---- Measurement aid (not part of the linear): the int8 matrix-core ceiling on given
+ * operands. The sustained rate of v_mfma_i32_32x32x32_i8 depends on the operand bits
+ * (the clock drops under the matrix cores' switching power), so the datasheet peak is
+ * not reachable on every input. This call replays the GEMM's per-K-step MFMA sequence
+ * of its 160 x 256 tile (per wavefront, 2 weight x 5 token fragments) on fragments of
+ * xq [M,K] and wq [N,K] held in registers: 256 workgroups of 4 wavefronts, each loading
+ * 8 K-steps of its tile's fragments (rows and channels wrapped modulo M and N), then
+ * `iters` sweeps over them with no memory traffic. Its rate, w8a8_mfma_ceiling_ops(iters)
+ * / launch time, is the matrix-core ceiling for these codes.
+ *   wave_sums: [1024] uint32 on the device; wavefront w of workgroup b writes entry
+ *              4b + w, the sum of its accumulator elements modulo 2^32 (a checksum).
+ * Needs K % 32 == 0 (else W8A8_ERR_SHAPE), 16-byte aligned xq and wq and 1 <= iters <=
+ * W8A8_CEILING_MAX_ITERS (else W8A8_ERR_ARG). w8a8_mfma_ceiling_ops returns the int8
+ * ops (2 per multiply-accumulate) of one launch, or -1 for iters out of range. */
+#define W8A8_CEILING_MAX_ITERS 1000000
+int64_t w8a8_mfma_ceiling_ops(int64_t iters);
+w8a8_status w8a8_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int64_t N,
+                              int64_t K, int64_t iters, uint32_t *wave_sums, void *stream);
+
 /* Static description of a status code. */
 const char *w8a8_status_string(w8a8_status status);
 

@@ -32,7 +32,7 @@ __all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
            "col_absmax", "smooth_factors", "ACTS",
            "tile_count", "tile_name", "select_tile", "default_tile", "gemm_workspace_bytes",
            "linear_workspace_bytes", "library_path", "load_library", "W8A8Error",
-           "MAX_K", "version"]
+           "MAX_K", "version", "mfma_ceiling", "mfma_ceiling_ops"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libw8a8.so")
@@ -84,6 +84,8 @@ def load_library():
         "w8a8_default_tile": ([I64, I64, I64], INT),
         "w8a8_status_string": ([INT], ctypes.c_char_p),
         "w8a8_version": ([], ctypes.c_char_p),
+        "w8a8_mfma_ceiling_ops": ([I64], I64),
+        "w8a8_mfma_ceiling": ([P, P, I64, I64, I64, I64, P, P], INT),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -327,3 +329,33 @@ def gemm_acc_i32(xq, wq, *, tile: int = -1, out=None):
         _call("w8a8_gemm_acc_i32_ex", _ptr(xq), _ptr(wq), _ptr(acc), M, N, K, int(tile),
               _stream(xq.device))
     return acc
+
+
+def mfma_ceiling_ops(iters: int) -> int:
+    """Int8 ops (2 per multiply-accumulate) of one mfma_ceiling launch."""
+    n = int(load_library().w8a8_mfma_ceiling_ops(int(iters)))
+    if n < 0:
+        raise ValueError(f"iters out of range: {iters}")
+    return n
+
+
+def mfma_ceiling(xq, wq, iters: int, *, out=None):
+    """Measurement aid: the GEMM's MFMA sequence replayed from registers on fragments
+    of xq [M,K] / wq [N,K] (K % 32 == 0), `iters` sweeps. Returns the per-wavefront
+    checksums (int32 [1024], the uint32 sums of the accumulators); its launch time
+    against mfma_ceiling_ops(iters) is the matrix-core ceiling on these codes."""
+    _check(xq, torch.int8, 2, "xq")
+    _check(wq, torch.int8, 2, "wq")
+    _same_device(xq, wq)
+    M, K = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != K:
+        raise ValueError("shape mismatch")
+    sums = out if out is not None else torch.empty(1024, dtype=torch.int32, device=xq.device)
+    _check(sums, torch.int32, 1, "out")
+    if sums.numel() < 1024:
+        raise ValueError("out needs 1024 entries")
+    with torch.cuda.device(xq.device):
+        _call("w8a8_mfma_ceiling", _ptr(xq), _ptr(wq), M, N, K, int(iters), _ptr(sums),
+              _stream(xq.device))
+    return sums

@@ -30,7 +30,7 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC", "-fvisibility=h
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-command-line-argument"]
 
-SOURCES = ["quant_rows.hip", "gemm_i8.hip", "w8a8_api.hip"]
+SOURCES = ["quant_rows.hip", "gemm_i8.hip", "mfma_ceiling.hip", "w8a8_api.hip"]
 
 
 def _compile(src: str, extra: list[str]) -> str:

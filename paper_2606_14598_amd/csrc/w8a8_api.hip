@@ -273,6 +273,25 @@ const char *w8a8_status_string(w8a8_status status) {
     }
 }
 
+int64_t w8a8_mfma_ceiling_ops(int64_t iters) {
+    return iters < 1 || iters > W8A8_CEILING_MAX_ITERS ? -1 : mfma_ceiling_ops(iters);
+}
+
+w8a8_status w8a8_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int64_t N,
+                              int64_t K, int64_t iters, uint32_t *wave_sums, void *stream) {
+    if (!xq || !wq || !wave_sums)
+        return W8A8_ERR_NULL;
+    if (M < 1 || N < 1 || K < 32 || K % 32 != 0 || !product_ok(M, K) || !product_ok(N, K))
+        return W8A8_ERR_SHAPE;
+    if (K > W8A8_MAX_K)
+        return W8A8_ERR_K_OVERFLOW;
+    if (iters < 1 || iters > W8A8_CEILING_MAX_ITERS || !aligned16(xq) || !aligned16(wq) ||
+        reinterpret_cast<uintptr_t>(wave_sums) % 4 != 0)
+        return W8A8_ERR_ARG;
+    return from_hip(launch_mfma_ceiling(xq, wq, M, N, K, (int)iters, wave_sums,
+                                        as_stream(stream)));
+}
+
 const char *w8a8_version(void) { return "w8a8-gfx950 0.1.0"; }
 
 }  // extern "C"

@@ -59,4 +59,12 @@ size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,
                        size_t ws_bytes, hipStream_t stream);
 
+// ---------------------------------------------------------------- measurement aid
+// Int8 ops (2 per multiply-accumulate) of one launch of the matrix-core ceiling kernel.
+int64_t mfma_ceiling_ops(int64_t iters);
+// The GEMM's MFMA sequence replayed from registers on fragments of xq / wq (K % 32 == 0,
+// 16-byte aligned), iters sweeps; one uint32 checksum per wavefront into wave_sums[1024].
+hipError_t launch_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int64_t N,
+                               int64_t K, int iters, uint32_t *wave_sums, hipStream_t s);
+
 }  // namespace w8a8

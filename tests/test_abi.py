@@ -196,3 +196,17 @@ def test_default_tile_follows_the_wave_cost_model(lib):
         name = lib.w8a8_tile_name(lib.w8a8_default_tile(M, 128, 4096)).decode()
         assert name.startswith("skinny"), (M, name)
     assert lib.w8a8_default_tile(0, 8, 8) == -1
+
+
+def test_mfma_ceiling_validation(lib):
+    P = ctypes.c_void_p
+    fake = P(256)  # never dereferenced: validation fails first
+    assert lib.w8a8_mfma_ceiling(None, fake, 4, 4, 64, 1, fake, None) == ERR_NULL
+    assert lib.w8a8_mfma_ceiling(fake, fake, 4, 4, 64, 1, None, None) == ERR_NULL
+    assert lib.w8a8_mfma_ceiling(fake, fake, 4, 4, 48, 1, fake, None) == ERR_SHAPE   # K % 32
+    assert lib.w8a8_mfma_ceiling(fake, fake, 0, 4, 64, 1, fake, None) == ERR_SHAPE
+    assert lib.w8a8_mfma_ceiling(fake, fake, 4, 4, 64, 0, fake, None) == ERR_ARG
+    assert lib.w8a8_mfma_ceiling(P(264), fake, 4, 4, 64, 1, fake, None) == ERR_ARG  # alignment
+    # ops of one launch: 256 workgroups x 4 wavefronts x 8 K-steps x 10 MFMAs x 65536 ops
+    assert lib.w8a8_mfma_ceiling_ops(3) == 256 * 4 * 3 * 8 * 10 * 65536
+    assert lib.w8a8_mfma_ceiling_ops(0) == -1

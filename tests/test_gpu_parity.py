@@ -374,3 +374,42 @@ def test_split_k_tiles_exact(M, N, K):
         assert np.array_equal(y, y_o), w8a8.tile_name(t)
         acc = host(w8a8.gemm_acc_i32(xq, wq, tile=t))   # runs unsplit
         assert np.array_equal(acc, oracle.gemm_acc(xq_o, wq_o)), w8a8.tile_name(t)
+
+
+# ---------------------------------------------------------------- measurement aid
+
+def _ceiling_checksums(xq, wq, iters):
+    """Per-wavefront sum of accumulators of the ceiling kernel, from its definition:
+    iters * sum over K-steps s and k < 32 of (sum of the wavefront's 64 weight rows at
+    k_s + k) * (sum of its 160 token rows at k_s + k), modulo 2^32."""
+    M, K = xq.shape
+    N = wq.shape[0]
+    x64, w64 = xq.astype(np.int64), wq.astype(np.int64)
+    out = np.zeros(1024, dtype=np.int64)
+    for b in range(256):
+        tm, tn = b // 16, b % 16
+        ks = [((b * 8 + s) % (K // 32)) * 32 for s in range(8)]
+        rows_m = [(tm * 160 + r) % M for r in range(160)]
+        colx = x64[rows_m].sum(axis=0)
+        for w in range(4):
+            rows_n = [(tn * 256 + w * 64 + r) % N for r in range(64)]
+            colw = w64[rows_n].sum(axis=0)
+            tot = sum(int((colw[k:k + 32] * colx[k:k + 32]).sum()) for k in ks)
+            out[b * 4 + w] = (iters * tot) % (1 << 32)
+    return out
+
+
+@pytest.mark.parametrize("M,N,K", [(2560, 4096, 4096), (77, 130, 96)])
+def test_mfma_ceiling_checksums(M, N, K):
+    """The matrix-core ceiling probe computes what it claims: its per-wavefront
+    accumulator sums equal the closed form on the same codes (so the timed MFMAs are
+    real work on the given operands)."""
+    say(f"mfma ceiling M={M} N={N} K={K}")
+    rng = np.random.default_rng(M + N + K)
+    xq = rng.integers(-127, 128, size=(M, K), dtype=np.int8)
+    wq = rng.integers(-127, 128, size=(N, K), dtype=np.int8)
+    base = _ceiling_checksums(xq, wq, 1)
+    for iters in (1, 3):
+        sums = w8a8.mfma_ceiling(torch.from_numpy(xq).cuda(), torch.from_numpy(wq).cuda(), iters)
+        got = host(sums).astype(np.int64) % (1 << 32)
+        assert np.array_equal(got, (iters * base) % (1 << 32)), iters
