@@ -229,34 +229,40 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
         if (t == 0)
             scale[row] = rs.scale;
         uint2 *dst = reinterpret_cast<uint2 *>(q + row * K);
-        uint2 cv[NV];
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
+        // Codes of vector j of this lane (8 bytes).
+        auto codes = [&](int j) __attribute__((always_inline)) {
+            uint2 o;
             if constexpr (PLAIN) {
-                cv[j] = code8(d[j], rs.inv);
+                o = code8(d[j], rs.inv);
             } else {
                 uint32_t c[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     c[e] = code_f(f[j][e], rs.inv);
-                cv[j].x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-                cv[j].y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
+                o.x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+                o.y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
             }
-        }
-        if (NV % 2 == 0 && wide) {
-            // 16-byte streaming stores (K % 16 == 0, q 16-byte aligned). Vectors j and
-            // j+1 of lane t are j*TPR + t and (j+1)*TPR + t; neighbouring lanes swap one
-            // code word pair so that the even lane holds vectors j*TPR + t, +1 and the
-            // odd lane (j+1)*TPR + t - 1, +1. Streaming 16-byte stores leave no dirty
-            // lines in this XCD's L2 for the kernel's end to write back before the
-            // consumer starts (plain stores, and 8-byte streaming ones, delayed the next
-            // kernel by 1.5-2.5 us).
+            return o;
+        };
+        // The paired path for the plain rule, and for transformed rows with two vectors
+        // per thread; with more, transformed rows measured 3-12% slower with it (GELU and
+        // multiplier variants at K = 12288 and 16384) and keep 8-byte stores.
+        constexpr bool PAIRS = NV % 2 == 0 && (PLAIN || NV <= 2);
+        if (PAIRS && wide) {
+            // 16-byte streaming stores (K % 16 == 0, q 16-byte aligned), one pair of
+            // vectors at a time. Vectors j and j+1 of lane t are j*TPR + t and
+            // (j+1)*TPR + t; neighbouring lanes swap one code word pair so that the even
+            // lane holds vectors j*TPR + t, +1 and the odd lane (j+1)*TPR + t - 1, +1.
+            // Streaming 16-byte stores leave no dirty lines in this XCD's L2 for the
+            // kernel's end to write back before the consumer starts (plain stores, and
+            // 8-byte streaming ones, delayed the next kernel by 1.5-2.5 us).
             const bool odd = t & 1;
 #pragma unroll
             for (int j = 0; j + 1 < NV; j += 2) {
                 // Selects on scalars (a select between array elements would put the
                 // array in memory).
-                const uint32_t a0 = cv[j].x, a1 = cv[j].y, b0 = cv[j + 1].x, b1 = cv[j + 1].y;
+                const uint2 ca = codes(j), cb = codes(j + 1);
+                const uint32_t a0 = ca.x, a1 = ca.y, b0 = cb.x, b1 = cb.y;
                 const uint32_t r0 = swap_lane_pair(odd ? a0 : b0);
                 const uint32_t r1 = swap_lane_pair(odd ? a1 : b1);
                 const int64_t v0 = (int64_t)(odd ? j + 1 : j) * TPR + t - (odd ? 1 : 0);
@@ -271,7 +277,7 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
             for (int j = 0; j < NV; ++j) {
                 const int64_t vi = (int64_t)j * TPR + t;
                 if (vi < nvec)
-                    dst[vi] = cv[j];
+                    dst[vi] = codes(j);
             }
         }
     };
