@@ -92,7 +92,11 @@ size_t w8a8_gemm_workspace_bytes_ex(int64_t M, int64_t N, int64_t K, int tile_id
  * fused GEMM (steps 2 and 3). wq / w_scale come from w8a8_quantize_weight.
  * workspace: at least w8a8_linear_workspace_bytes(M,N,K) bytes, 256-byte aligned; it
  * holds Xq [M,K] and sx [M] (and whatever the GEMM needs) and may be reused once the
- * call's work on `stream` has finished. */
+ * call's work on `stream` has finished. With few tokens (the GEMM tile streams the
+ * weight, K % 16 == 0, 16-byte aligned x and wq, and a short quantization per
+ * workgroup) quantizer and GEMM run as one launch, each workgroup quantizing its own
+ * token rows into LDS with the same arithmetic; the workspace is then left untouched
+ * and the result is the same. */
 w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scale,
                         const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
                         int64_t K, void *workspace, size_t workspace_bytes,

@@ -27,6 +27,7 @@
 // run touches stay in that XCD's L2. The integer accumulation is exact, so every tile,
 // split and order gives identical bits.
 #include "w8a8_internal.hpp"
+#include "quant_math.hpp"
 
 #include <utility>
 
@@ -106,6 +107,7 @@ struct KParams {
     int k_chunk;     // K bytes per split (a multiple of BK; K when unsplit)
     int part_vec;    // partial rows 16-byte aligned (N % 4 == 0)
     int32_t *part;   // k_split > 1: int32 partials [k_split][M][N]
+    const uint16_t *x;   // the small fused linear: bf16 X [M,K] (a.xq, a.sx unused)
 };
 
 // Epilogue of one wavefront's (FN*32 channels) x (FM*32 tokens) accumulator tile whose
@@ -765,13 +767,21 @@ gemm_i8_lds_kernel(KParams kp) {
 // tokens). Partial accumulators are summed across wavefronts in LDS (integer, exact),
 // then the epilogue runs as in the tiled kernels: lane l of a 16x16 accumulator holds
 // token l % 16 and channels 4(l / 16) + e.
-template <int FMB, int FNB, int NW, int EPI>
+//
+// QX (the small fused linear): the workgroup first quantizes its own token rows of the
+// bf16 X with the row quantizer's arithmetic (two passes over each row: the absmax,
+// then the codes) into LDS, rows of K + 16 bytes, and their scales; the product then
+// reads the token fragments and the epilogue the scales from there. The linear is then
+// one launch. Each token block is quantized by every channel block that uses it, which
+// the host allows only while those repeated reads of X stay small.
+template <int FMB, int FNB, int NW, int EPI, bool QX = false>
 __global__ void __launch_bounds__(NW * 64)
 gemm_i8_skinny_kernel(KParams kp) {
     const GemmArgs &a = kp.a;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15, g = lane >> 4;
+    extern __shared__ __attribute__((aligned(16))) int8_t qx_lds[];
     // Workgroup b: channel block b % tiles_n, token block b / tiles_n (more than one
     // token block only when more than 16 * FMB tokens are forced onto this kernel).
     const int64_t n0 = (int64_t)(blockIdx.x % kp.tiles_n) * (16 * FNB);
@@ -784,6 +794,27 @@ gemm_i8_skinny_kernel(KParams kp) {
         (void *)(a.wq + n0 * K), (short)0, rows_w * K, kRsrcWord3);
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(a.xq + mb * K), (short)0, rows_x * K, kRsrcWord3);
+    // QX: codes of token row i at qx_lds + i * QS, its scale at qx_scale[i].
+    const int QS = K + 16;
+    float *const qx_scale = reinterpret_cast<float *>(qx_lds + rows_x * QS);
+    if constexpr (QX) {
+        // One wavefront per row: the absmax pass, then the codes (the row is read again,
+        // from cache).
+        const int nvec = K >> 3;
+        for (int i = wave; i < rows_x; i += NW) {
+            const uint4 *src = reinterpret_cast<const uint4 *>(kp.x + (mb + i) * (int64_t)K);
+            uint32_t mx = 0;
+            for (int vi = lane; vi < nvec; vi += 64)
+                mx = max(mx, qmath::absmax8(src[vi]));
+            mx = qmath::wave_max(mx);
+            const qmath::RowScale rs = qmath::row_scale(mx);
+            for (int vi = lane; vi < nvec; vi += 64)
+                *reinterpret_cast<uint2 *>(qx_lds + i * QS + vi * 8) = qmath::code8(src[vi], rs.inv);
+            if (lane == 0)
+                qx_scale[i] = rs.scale;
+        }
+        __syncthreads();
+    }
 
     i32x4 acc[FNB][FMB];
 #pragma unroll
@@ -812,8 +843,15 @@ gemm_i8_skinny_kernel(KParams kp) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 const int k = kb + s * 64;
-                const int off = (k < K && m < rows_x) ? m * K + k : kOOB;
-                xv[s] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+                if constexpr (QX) {
+                    xv[s] = (k < K && m < rows_x)
+                                ? *reinterpret_cast<const i32x4 *>(qx_lds + m * QS + k)
+                                : i32x4{0, 0, 0, 0};
+                } else {
+                    const int off = (k < K && m < rows_x) ? m * K + k : kOOB;
+                    xv[s] = __builtin_bit_cast(
+                        i32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+                }
             }
 #pragma unroll
             for (int c = 0; c < FNB; ++c)
@@ -852,7 +890,7 @@ gemm_i8_skinny_kernel(KParams kp) {
             }
         } else {
             uint16_t *o = static_cast<uint16_t *>(a.out) + m * N + n;
-            const float sxm = a.sx[m];
+            const float sxm = QX ? qx_scale[b * 16 + r] : a.sx[m];
             uint16_t hv[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -970,10 +1008,17 @@ struct SkinnyTile {
     static constexpr int lds = NW * FNB * FMB * 64 * 16;
     static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
         const dim3 grid((unsigned)(kp.tiles_m * kp.tiles_n)), block(threads);
-        if (epi == EPI_BF16)
+        if (kp.x) {
+            // The small fused linear: LDS for the token block's codes and scales.
+            const int rows = (int)(kp.a.M < 16 * FMB ? kp.a.M : 16 * FMB);
+            const size_t dyn = (size_t)rows * (kp.a.K + 16) + (size_t)rows * 4;
+            hipLaunchKernelGGL((gemm_i8_skinny_kernel<FMB, FNB, NW, EPI_BF16, true>), grid, block,
+                               dyn, s, kp);
+        } else if (epi == EPI_BF16) {
             hipLaunchKernelGGL((gemm_i8_skinny_kernel<FMB, FNB, NW, EPI_BF16>), grid, block, 0, s, kp);
-        else
+        } else {
             hipLaunchKernelGGL((gemm_i8_skinny_kernel<FMB, FNB, NW, EPI_I32>), grid, block, 0, s, kp);
+        }
         return hipGetLastError();
     }
 };
@@ -1000,7 +1045,7 @@ struct TileEntry {
 #define W8A8_TILE(NAME, TM, TN, BK, WM, WN, GM, S)                                          \
     TileEntry {                                                                              \
         {NAME, TM, TN, BK, Tile<TM, TN, BK, WM, WN, S>::threads,                            \
-         Tile<TM, TN, BK, WM, WN, S>::lds, 1, -1},                                           \
+         Tile<TM, TN, BK, WM, WN, S>::lds, 1, -1, 0},                                        \
             GM, &Tile<TM, TN, BK, WM, WN, S>::launch                                         \
     }
 
@@ -1008,14 +1053,14 @@ struct TileEntry {
 #define W8A8_TILE_SPLIT(NAME, TM, TN, BK, WM, WN, GM, S, KSPLIT, BASE)                    \
     TileEntry {                                                                              \
         {NAME, TM, TN, BK, Tile<TM, TN, BK, WM, WN, S>::threads,                            \
-         Tile<TM, TN, BK, WM, WN, S>::lds, KSPLIT, BASE},                                    \
+         Tile<TM, TN, BK, WM, WN, S>::lds, KSPLIT, BASE, 0},                                 \
             GM, &Tile<TM, TN, BK, WM, WN, S>::launch                                         \
     }
 
 #define W8A8_SKINNY(NAME, FMB, FNB, NW)                                                  \
     TileEntry {                                                                              \
         {NAME, 16 * FMB, 16 * FNB, 256, SkinnyTile<FMB, FNB, NW>::threads,                  \
-         SkinnyTile<FMB, FNB, NW>::lds, 1, -1},                                              \
+         SkinnyTile<FMB, FNB, NW>::lds, 1, -1, 1},                                           \
             1, &SkinnyTile<FMB, FNB, NW>::launch                                             \
     }
 
@@ -1157,6 +1202,60 @@ size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K) {
     return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
 }
 
+// The small fused linear (see gemm_i8_skinny_kernel, QX): the chosen tile streams the
+// weight, K % 16 == 0 with 16-byte aligned operands, a token block's codes and scales fit
+// in 48 KB of LDS, and the repeated reads of X (once per channel block) total at most
+// 16 MB.
+bool linear_small_applies(int64_t M, int64_t N, int64_t K, const void *x, const void *wq) {
+    if (M <= 0 || N <= 0 || K <= 0 || K % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(wq) % 16 != 0)
+        return false;
+    const TileInfo &t = kTiles[select_tile(M, N, K)].info;
+    if (!t.streaming)
+        return false;
+    const int64_t rows = M < t.tm ? M : t.tm;
+    if (rows * (K + 16) + rows * 4 > 48 * 1024)
+        return false;
+    // The quantization is a serial chain per wavefront (one row per wavefront, its
+    // 16-byte vectors strided over the lanes, two passes): past 7 vectors per lane it
+    // costs more than the separate quantizer launch it saves (measured: M = 1 at K =
+    // 3136 fused is faster, at K = 4096 slower).
+    const int64_t nw = t.threads / 64;
+    if ((K / 8 + 63) / 64 * ((rows + nw - 1) / nw) > 7)
+        return false;
+    const int64_t channel_blocks = (N + t.tn - 1) / t.tn;
+    return channel_blocks * M * K * 2 <= ((int64_t)16 << 20);
+}
+
+hipError_t launch_linear_small(const uint16_t *x, const int8_t *wq, const float *sw,
+                               const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                               int64_t K, hipStream_t stream) {
+    const TileEntry &t = kTiles[select_tile(M, N, K)];
+    KParams kp;
+    kp.a.xq = nullptr;
+    kp.a.wq = wq;
+    kp.a.sx = nullptr;
+    kp.a.sw = sw;
+    kp.a.bias = bias;
+    kp.a.out = y;
+    kp.a.M = M;
+    kp.a.N = N;
+    kp.a.K = K;
+    kp.tiles_m = (int)((M + t.info.tm - 1) / t.info.tm);
+    kp.tiles_n = (int)((N + t.info.tn - 1) / t.info.tn);
+    kp.gm = t.gm;
+    const bool ov = (N % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 8 == 0) &&
+                    (reinterpret_cast<uintptr_t>(sw) % 16 == 0) &&
+                    (bias == nullptr || reinterpret_cast<uintptr_t>(bias) % 8 == 0);
+    kp.out_vec = ov ? 1 : 0;
+    kp.k_split = 1;
+    kp.k_chunk = (int)K;
+    kp.part = nullptr;
+    kp.part_vec = 0;
+    kp.x = x;
+    return t.launch(EPI_BF16, kp, stream);
+}
+
 hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,
                        size_t ws_bytes, hipStream_t stream) {
     const TileEntry &t = kTiles[id];
@@ -1180,6 +1279,7 @@ hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *
     kp.k_chunk = (int)a.K;
     kp.part = nullptr;
     kp.part_vec = 0;
+    kp.x = nullptr;
     if (!vec)
         return GenericTile::launch(epi, kp, stream);
     if (t.info.ksplit > 1) {

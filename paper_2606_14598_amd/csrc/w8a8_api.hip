@@ -201,6 +201,9 @@ w8a8_status w8a8_linear_ex(const uint16_t *x, int act, const float *col_mul,
                                           align_up((size_t)(M * K)));
     char *gws = reinterpret_cast<char *>(sx) + align_up((size_t)M * sizeof(float));
     hipStream_t s = as_stream(stream);
+    // Few tokens, plain rule: quantizer and GEMM in one launch (the workspace is unused).
+    if (act == W8A8_ACT_NONE && !col_mul && linear_small_applies(M, N, K, x, wq))
+        return from_hip(launch_linear_small(x, wq, w_scale, bias, y, M, N, K, s));
     hipError_t e = launch_quant_rows(x, M, K, act, col_mul, xq, sx, s);
     if (e != hipSuccess)
         return W8A8_ERR_HIP;

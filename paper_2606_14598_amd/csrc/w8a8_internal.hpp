@@ -44,6 +44,7 @@ struct TileInfo {
     int lds_bytes;       // static LDS per workgroup
     int ksplit;          // K divided among this many workgroups per tile (1: no split)
     int base;            // for a split tile, the id of the same tile unsplit (else -1)
+    int streaming;       // 1: the weight-streaming kernel for few tokens
 };
 
 int tile_count();
@@ -58,6 +59,14 @@ size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K);
 // Launch tile `id` with epilogue `epi`; `vec` selects the 16-byte-aligned load path.
 hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *ws,
                        size_t ws_bytes, hipStream_t stream);
+
+// The small fused linear: quantizer and GEMM in one launch, for shapes whose chosen tile
+// is a weight-streaming one and whose token blocks are small enough to be quantized by
+// every workgroup that uses them (plain rule only: no transform, no multiplier).
+bool linear_small_applies(int64_t M, int64_t N, int64_t K, const void *x, const void *wq);
+hipError_t launch_linear_small(const uint16_t *x, const int8_t *wq, const float *sw,
+                               const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                               int64_t K, hipStream_t stream);
 
 // ---------------------------------------------------------------- measurement aid
 // Int8 ops (2 per multiply-accumulate) of one launch of the matrix-core ceiling kernel.

@@ -413,3 +413,58 @@ def test_mfma_ceiling_checksums(M, N, K):
         sums = w8a8.mfma_ceiling(torch.from_numpy(xq).cuda(), torch.from_numpy(wq).cuda(), iters)
         got = host(sums).astype(np.int64) % (1 << 32)
         assert np.array_equal(got, (iters * base) % (1 << 32)), iters
+
+
+# ---------------------------------------------------------------- small fused linear
+
+# (M, K, N, fused): few tokens whose tile streams the weight run quantizer and GEMM in
+# one launch (the workspace stays untouched); the rest keep the two-launch path: a tile
+# that does not stream the weight (M = 1, N = 16384 picks a tiled kernel; M = 77, 2560),
+# a token block over the LDS budget (13 x 4112), more than 7 vectors per lane to
+# quantize (K = 4096), K % 16 != 0 (264).
+SMALL_FUSED = [(64, 256, 128, True), (1, 4096, 4096, False), (1, 4096, 16384, False),
+               (1, 3136, 4096, True), (5, 1024, 520, True), (16, 2048, 4096, True),
+               (13, 3088, 80, True), (13, 4112, 80, False), (77, 3136, 4096, False),
+               (2560, 256, 64, False), (3, 264, 64, False)]
+
+
+@pytest.mark.parametrize("M,K,N,fused", SMALL_FUSED)
+def test_small_fused_linear(M, K, N, fused):
+    """The one-launch linear for few tokens gives the two-launch path's bits (codes,
+    scales and accumulator exact, so the same bf16 output) and the oracle's."""
+    say(f"small fused linear M={M} K={K} N={N} fused={fused}")
+    x, w, b = si.make_inputs((M, K, N), seed=3 * M + K + N, dist="student_t")
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, _, _, _ = oracle.linear(x, wq_o, sw_o, b)
+    xd, bd = dev_bf16(x), dev_bf16(b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    nws = w8a8.linear_workspace_bytes(M, N, K)
+    ws = torch.full((nws,), 0x5A, dtype=torch.uint8, device="cuda")
+    y = w8a8.linear(xd, wq, sw, bd, workspace=ws)
+    torch.cuda.synchronize()
+    untouched = bool((ws == 0x5A).all().item())
+    assert untouched == fused, (M, K, N, untouched)
+    xq, sx = w8a8.quantize_act(xd)
+    y2 = w8a8.gemm(xq, sx, wq, sw, bd)
+    assert np.array_equal(host_bits(y), host_bits(y2))
+    assert_bf16_parity(host_bits(y), y_o, f"small fused {M}x{K}x{N}")
+    # the same without bias
+    y3 = w8a8.linear(xd, wq, sw, None)
+    y4 = w8a8.gemm(xq, sx, wq, sw, None)
+    assert np.array_equal(host_bits(y3), host_bits(y4))
+
+
+def test_small_fused_linear_zero_and_tiny_rows():
+    """Zero and tiny token rows in the fused path: codes and scales 0, so y = bias."""
+    M, K, N = 4, 512, 256
+    x, w, b = si.make_inputs((M, K, N), seed=11)
+    x = x.copy()
+    x[0] = 0                                  # a zero row
+    x[1] = 0x0080                             # tiny positive values (bf16 1.2e-38): 127/a overflows
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    y = w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b))
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, _, sx_o, _ = oracle.linear(x, wq_o, sw_o, b)
+    assert sx_o[0] == 0 and sx_o[1] == 0
+    assert np.array_equal(host_bits(y)[:2], np.stack([b, b]))
+    assert_bf16_parity(host_bits(y), y_o, "fused zero/tiny rows")
