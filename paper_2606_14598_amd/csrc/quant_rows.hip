@@ -154,11 +154,14 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
             m = __float_as_uint(fm);   // |v| >= 0: its bit pattern orders like the value
         }
         m = wave_max(m);
-        if constexpr (TPR == 256) {
+        if constexpr (TPR > 64) {
+            constexpr int WPR = TPR / 64;   // wavefronts per row
             if ((threadIdx.x & 63) == 0)
-                part[sub][(threadIdx.x >> 6) & 3] = m;
+                part[sub][(threadIdx.x >> 6) % WPR] = m;
             __syncthreads();
-            m = max(max(part[sub][0], part[sub][1]), max(part[sub][2], part[sub][3]));
+#pragma unroll
+            for (int w = 0; w < WPR; ++w)
+                m = max(m, part[sub][w]);
             __syncthreads();   // part is rewritten by the next row group
         }
         const RowScale rs = PLAIN ? row_scale(m) : row_scale_f(__uint_as_float(m));
@@ -314,12 +317,20 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 256)
             return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        // K in (2048, 4096]: a wavefront per row, or the whole block per row when there
-        // are too few rows to fill the chip with one-wavefront rows (measured crossover
-        // near 4096 rows).
-        if (nvec <= 512)
-            return rows < 4096 ? launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s)
-                               : launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        // K in (2048, 4096]: a wavefront per row, or more threads per row when there are
+        // too few rows to fill the chip with one-wavefront rows (measured crossover near
+        // 4096 rows): two wavefronts per row for the plain rule (two rows per block, so
+        // 2560 rows need no second round of blocks: 5% faster than a block per row), the
+        // whole block for transformed rows (whose 16-byte store pairs need two vectors
+        // per thread).
+        if (nvec <= 512) {
+            if (rows >= 4096)
+                return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            if constexpr (PLAIN)
+                return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            else
+                return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        }
         if (nvec <= 1024)
             return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 2048)

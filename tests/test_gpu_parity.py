@@ -73,7 +73,7 @@ def test_quantizer_bytes_and_scales_exact(K):
 @pytest.mark.parametrize("K", [2056, 3136, 4096])
 def test_quantizer_many_rows_exact(K):
     """At 4096 rows and more, K in (2048, 4096] takes one wavefront per row (fewer rows
-    take the whole block per row): both variants against the oracle."""
+    take two wavefronts per row, two rows per block): both variants against the oracle."""
     x, _, _ = si.make_inputs((4200, K, 1), seed=700 + K, dist="student_t")
     x[4099] = 0
     q_o, s_o = oracle.quantize_rows(x)
