@@ -18,7 +18,7 @@
 // second (quantizing) pass and written with 8-byte stores, by a persistent grid that
 // prefetches the next rows while it finishes the current ones; the row maximum is taken
 // on the bf16 bit patterns (|v| ordered as an unsigned integer, exact for finite values)
-// with a wavefront butterfly and, for 256-thread rows, one LDS exchange.
+// with a wavefront butterfly and, for rows of several wavefronts, one LDS exchange.
 #include "w8a8_internal.hpp"
 #include "quant_math.hpp"
 
@@ -83,21 +83,25 @@ __device__ __forceinline__ uint32_t abs_bits(float v) {
 }
 
 // Register-resident path, persistent and software-pipelined: TPR threads per row
-// (64 = one wavefront, 256 = the block), NV 16-byte vectors per thread (K % 8 == 0,
-// v 16-byte and q 8-byte aligned). Row group j of a block holds rows j*RPB .. j*RPB +
-// RPB - 1; block b handles row groups b, b + G, b + 2G, ... (G = gridDim.x) and loads
+// (64 = one wavefront, up to 1024 = the block), NV 16-byte vectors per thread (K % 8 ==
+// 0, v 16-byte and q 8-byte aligned). Blocks have max(TPR, 256) threads. Row group j of
+// a block holds rows j*RPB .. j*RPB + RPB - 1; block b handles row groups b, b + G, b +
+// 2G, ... (G = gridDim.x) and loads
 // group j + G while it reduces, quantizes and stores group j, so the HBM reads of the
 // next rows overlap the work and the stores of the current ones.
 // With a transform (ACT != ACT_NONE or a multiplier), each thread's columns are the
 // same for every row, so its multipliers are loaded once into registers; the
 // transformed row is held as float32 between the maximum and the coding pass.
+template <int TPR>
+constexpr int reg_block_threads() { return TPR > 256 ? TPR : 256; }
+
 template <int TPR, int NV, int ACT, bool CM>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(reg_block_threads<TPR>())
 quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
                const float *__restrict__ colmul, int8_t *__restrict__ q,
                float *__restrict__ scale) {
     constexpr bool PLAIN = ACT == ACT_NONE && !CM;
-    constexpr int RPB = 256 / TPR;
+    constexpr int RPB = reg_block_threads<TPR>() / TPR;
     const int t = threadIdx.x % TPR;
     const int sub = threadIdx.x / TPR;
     const int64_t nvec = K >> 3;
@@ -237,27 +241,55 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
 }
 
 // General path: one 256-thread block per row, two passes over the row (the second
-// re-reads it, normally from L2). VEC selects 16-byte loads (K % 8 == 0 and aligned
-// pointers, plain rule only); otherwise every element is loaded and stored on its own,
-// for any K and any alignment, and a transform is evaluated in both passes.
+// re-reads it, normally from L2). VEC selects 16-byte loads and 8-byte stores (K % 8 ==
+// 0; v and colmul 16-byte, q 8-byte aligned); a transform is then evaluated on the 8
+// values of a vector in both passes. Otherwise every element is loaded and stored on
+// its own, for any K and any alignment.
 template <bool VEC, int ACT, bool CM>
 __global__ void __launch_bounds__(256)
 quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
                 const float *__restrict__ colmul, int8_t *__restrict__ q,
                 float *__restrict__ scale) {
     constexpr bool PLAIN = ACT == ACT_NONE && !CM;
-    static_assert(PLAIN || !VEC, "transformed rows take the element path");
     const int64_t row = blockIdx.x;
     const int t = threadIdx.x;
     const uint16_t *src = v + row * K;
+    const int64_t nvec = K >> 3;
     auto value = [&](int64_t k) {
         return transform<ACT, CM>(bf16_to_f32(src[k]), CM ? colmul[k] : 1.0f);
     };
+    // The 8 transformed values of vector vi.
+    auto values8 = [&](int64_t vi, float (&f)[8]) __attribute__((always_inline)) {
+        const uint4 d = reinterpret_cast<const uint4 *>(src)[vi];
+        float c[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+        if constexpr (CM) {
+            const float4 *c4 = reinterpret_cast<const float4 *>(colmul) + 2 * vi;
+            const float4 lo = c4[0], hi = c4[1];
+            c[0] = lo.x; c[1] = lo.y; c[2] = lo.z; c[3] = lo.w;
+            c[4] = hi.x; c[5] = hi.y; c[6] = hi.z; c[7] = hi.w;
+        }
+        const uint32_t w[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint32_t h = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
+            f[e] = transform<ACT, CM>(bf16_to_f32(h), c[e]);
+        }
+    };
     uint32_t m = 0;
-    if constexpr (VEC) {
+    if constexpr (VEC && PLAIN) {
         const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
-        for (int64_t vi = t; vi < (K >> 3); vi += 256)
+        for (int64_t vi = t; vi < nvec; vi += 256)
             m = max(m, absmax8(s4[vi]));
+    } else if constexpr (VEC) {
+        float fm = 0.0f;
+        for (int64_t vi = t; vi < nvec; vi += 256) {
+            float f[8];
+            values8(vi, f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                fm = fmaxf(fm, __builtin_fabsf(f[e]));
+        }
+        m = abs_bits(fm);
     } else if constexpr (PLAIN) {
         for (int64_t k = t; k < K; k += 256)
             m = max(m, (uint32_t)src[k] & 0x7FFFu);
@@ -275,11 +307,23 @@ quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
     if (t == 0)
         scale[row] = rs.scale;
     int8_t *dst = q + row * K;
-    if constexpr (VEC) {
+    if constexpr (VEC && PLAIN) {
         const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
         uint2 *d2 = reinterpret_cast<uint2 *>(dst);
-        for (int64_t vi = t; vi < (K >> 3); vi += 256)
+        for (int64_t vi = t; vi < nvec; vi += 256)
             d2[vi] = code8(s4[vi], rs.inv);
+    } else if constexpr (VEC) {
+        uint2 *d2 = reinterpret_cast<uint2 *>(dst);
+        for (int64_t vi = t; vi < nvec; vi += 256) {
+            float f[8];
+            values8(vi, f);
+            uint32_t c[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                c[e] = code_f(f[e], rs.inv);
+            d2[vi] = make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
+                                c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+        }
     } else if constexpr (PLAIN) {
         for (int64_t k = t; k < K; k += 256)
             dst[k] = (int8_t)code((uint32_t)src[k], rs.inv);
@@ -292,12 +336,14 @@ quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
 template <int TPR, int NV, int ACT, bool CM>
 hipError_t launch_reg(const uint16_t *v, int64_t rows, int64_t K, const float *colmul,
                       int8_t *q, float *scale, hipStream_t s) {
-    constexpr int RPB = 256 / TPR;
+    constexpr int BS = reg_block_threads<TPR>();
+    constexpr int RPB = BS / TPR;
     const int64_t groups = (rows + RPB - 1) / RPB;
-    // Persistent grid: a few blocks per CU, each walking row groups with prefetch.
-    const int64_t max_blocks = 256 * 8;
+    // Persistent grid: up to 2048 threads per CU, each block walking row groups with
+    // prefetch.
+    const int64_t max_blocks = 256 * 2048 / BS;
     const int64_t blocks = groups < max_blocks ? groups : max_blocks;
-    hipLaunchKernelGGL((quant_rows_reg<TPR, NV, ACT, CM>), dim3((unsigned)blocks), dim3(256),
+    hipLaunchKernelGGL((quant_rows_reg<TPR, NV, ACT, CM>), dim3((unsigned)blocks), dim3(BS),
                        0, s, v, rows, K, colmul, q, scale);
     return hipGetLastError();
 }
@@ -335,9 +381,19 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 2048)
             return launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        // Long rows (K up to 65536 for the plain rule, e.g. a 53248-wide projection
+        // input; 32768 for transformed rows, whose float32 copy of 8 vectors per thread
+        // would not fit 128 VGPRs): a 1024-thread block per row, still read once. The
+        // looped kernel below reads such rows twice, the second time mostly from the
+        // MALL, since 32 CUs' rows overflow an XCD's L2.
+        if (nvec <= 4096)
+            return launch_reg<1024, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if constexpr (PLAIN)
+            if (nvec <= 8192)
+                return launch_reg<1024, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
     }
-    if (PLAIN && vec)
-        hipLaunchKernelGGL((quant_rows_loop<PLAIN, ACT, CM>), dim3((unsigned)rows), dim3(256),
+    if (vec)
+        hipLaunchKernelGGL((quant_rows_loop<true, ACT, CM>), dim3((unsigned)rows), dim3(256),
                            0, s, v, rows, K, colmul, q, scale);
     else
         hipLaunchKernelGGL((quant_rows_loop<false, ACT, CM>), dim3((unsigned)rows), dim3(256),

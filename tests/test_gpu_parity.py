@@ -46,13 +46,14 @@ def say(*a):
 # ---------------------------------------------------------------- quantizer
 
 QUANT_K = [1, 3, 7, 8, 16, 24, 264, 512, 520, 1024, 2048, 3136, 4096, 4104, 8192, 16384,
-           16392, 20000]
+           16392, 20000, 32768, 32776, 53248, 65536, 65544, 65538]
 
 
 @pytest.mark.parametrize("K", QUANT_K)
 def test_quantizer_bytes_and_scales_exact(K):
     """Codes and scale bits equal the oracle's for every kernel variant (register-resident
-    wave/block rows, looped rows, scalar rows)."""
+    rows of one wavefront up to a 1024-thread block, K <= 65536; looped rows beyond;
+    scalar rows for K % 8 != 0)."""
     say(f"quantizer K={K}")
     x, _, _ = si.make_inputs((37, K, 1), seed=100 + K, dist="student_t")
     if K >= 4:
@@ -81,6 +82,20 @@ def test_quantizer_many_rows_exact(K):
     assert np.array_equal(host(q), q_o) and np.array_equal(host(s), s_o)
     q2, s2 = w8a8.quantize_act(dev_bf16(x[:4095]))
     assert np.array_equal(host(q2), q_o[:4095]) and np.array_equal(host(s2), s_o[:4095])
+
+
+@pytest.mark.parametrize("M,K", [(1100, 40000), (600, 24576)])
+def test_quantizer_long_rows_many_blocks(M, K):
+    """Rows of a 1024-thread block, more rows than the persistent grid's 512 blocks: each
+    block walks several rows with the next one prefetched; the zero row sits in a block's
+    second round."""
+    say(f"quantizer long rows M={M} K={K}")
+    x, _, _ = si.make_inputs((M, K, 1), seed=900 + K, dist="student_t")
+    x[M - 3] = 0
+    q_o, s_o = oracle.quantize_rows(x)
+    q, s = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(q), q_o)
+    assert np.array_equal(host(s).view(np.uint32), s_o.view(np.uint32))
 
 
 def test_quantizer_unaligned_pointers():

@@ -66,7 +66,8 @@ def check_gelu_codes(h_bits, q_g, s_g, q_o, s_o, cm=None, what=""):
 # ---------------------------------------------------------------- multiplier: exact
 
 CM_CASES = [(37, 8), (37, 24), (37, 264), (16, 1024), (9, 3136), (9, 4096), (5, 12288),
-            (5, 16384), (3, 20000), (37, 7), (11, 269), (8300, 512)]
+            (5, 16384), (3, 20000), (4, 32768), (3, 32776), (3, 40000), (37, 7), (11, 269),
+            (8300, 512)]
 
 
 @pytest.mark.parametrize("M,K", CM_CASES)
@@ -96,8 +97,8 @@ def test_colmul_unaligned_multiplier_takes_the_element_path():
 
 # ---------------------------------------------------------------- GELU: within bound
 
-GELU_CASES = [(37, 8), (37, 264), (64, 4096), (9, 16384), (5, 20000), (11, 269),
-              (8300, 512), (4100, 4096)]
+GELU_CASES = [(37, 8), (37, 264), (64, 4096), (9, 16384), (5, 20000), (4, 32768),
+              (3, 32776), (3, 53248), (11, 269), (8300, 512), (4100, 4096)]
 
 
 @pytest.mark.parametrize("M,K", GELU_CASES)
