@@ -192,7 +192,7 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
         // The paired path for the plain rule, and for transformed rows with two vectors
         // per thread; with more, transformed rows measured 3-12% slower with it (GELU and
         // multiplier variants at K = 12288 and 16384) and keep 8-byte stores.
-        constexpr bool PAIRS = NV % 2 == 0 && (PLAIN || NV <= 2);
+        constexpr bool PAIRS = PLAIN || NV == 2;
         if (PAIRS && wide) {
             // 16-byte streaming stores (K % 16 == 0, q 16-byte aligned), one pair of
             // vectors at a time. Vectors j and j+1 of lane t are j*TPR + t and
@@ -216,6 +216,20 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
                     __builtin_nontemporal_store(o, reinterpret_cast<u32x4v *>(dst + v0));
                 else if (v0 < nvec)
                     dst[v0] = make_uint2(o.x, o.y);
+            }
+            if constexpr (NV % 2 == 1) {
+                // The last vector of an odd count: the even lane of each pair takes its
+                // neighbour's codes (vector j*TPR + t + 1) and stores both.
+                const uint2 c = codes(NV - 1);
+                const uint32_t n0 = swap_lane_pair(c.x), n1 = swap_lane_pair(c.y);
+                const int64_t vi = (int64_t)(NV - 1) * TPR + t;
+                if (!odd) {
+                    if (vi + 1 < nvec)
+                        __builtin_nontemporal_store(u32x4v{c.x, c.y, n0, n1},
+                                                    reinterpret_cast<u32x4v *>(dst + vi));
+                    else if (vi < nvec)
+                        dst[vi] = c;
+                }
             }
         } else {
 #pragma unroll
@@ -356,6 +370,36 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
                      (reinterpret_cast<uintptr_t>(q) % 8 == 0) &&
                      (reinterpret_cast<uintptr_t>(colmul) % 16 == 0);
     const int64_t nvec = K / 8;
+    // The plain rule past 256 vectors per row: threads per row and vectors per thread
+    // from a sweep of both over rows x K (HIP-graph replays of the quantizer on its own;
+    // the rule keeps every choice within 7% of the sweep's best on the shapes measured).
+    // Fewer rows spread a row over more threads; the vector count per thread is the
+    // smallest that covers the row, so few lanes idle (at K = 4608 a 256 x 4 row leaves
+    // 44% of them idle: 11-24% slower than 128 x 5).
+    if constexpr (PLAIN) {
+        if (vec && nvec > 256 && nvec <= 2048) {
+            if (nvec <= 512) {
+                if (rows < 1024)
+                    return launch_reg<512, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                if (rows < 4096)
+                    return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            }
+            if (nvec <= 768 && rows < 1024)
+                return launch_reg<256, 3, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            if (nvec <= 640)
+                return launch_reg<128, 5, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            if (nvec <= 768)
+                return launch_reg<128, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            if (nvec <= 1024)
+                return rows < 4096 ? launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                                   : launch_reg<128, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            if (nvec <= 1536)
+                return launch_reg<256, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return rows < 2048 ? launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                               : launch_reg<1024, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        }
+    }
     if (vec && K > 0) {
         if (nvec <= 64)
             return launch_reg<64, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
@@ -363,19 +407,14 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 256)
             return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        // K in (2048, 4096]: a wavefront per row, or more threads per row when there are
-        // too few rows to fill the chip with one-wavefront rows (measured crossover near
-        // 4096 rows): two wavefronts per row for the plain rule (two rows per block, so
-        // 2560 rows need no second round of blocks: 5% faster than a block per row), the
-        // whole block for transformed rows (whose 16-byte store pairs need two vectors
+        // Transformed rows with K in (2048, 4096]: a wavefront per row, or the whole
+        // block when there are too few rows to fill the chip with one-wavefront rows
+        // (measured crossover near 4096 rows; its 16-byte store pairs need two vectors
         // per thread).
         if (nvec <= 512) {
             if (rows >= 4096)
                 return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            if constexpr (PLAIN)
-                return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            else
-                return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
         }
         if (nvec <= 1024)
             return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);

@@ -84,6 +84,35 @@ def test_quantizer_many_rows_exact(K):
     assert np.array_equal(host(q2), q_o[:4095]) and np.array_equal(host(s2), s_o[:4095])
 
 
+# (rows, K) covering each threads-per-row x vectors-per-thread choice of the plain rule
+# past 256 vectors per row, with a ragged last vector; K % 16 == 8 takes 8-byte stores,
+# K % 16 == 0 the 16-byte streaming stores (with an odd vector count, the last vector's
+# pair is stored by the even lane).
+ROW_MAPPINGS = [(37, 4096),     # 512 x 1
+                (300, 4104),    # 256 x 3, 8-byte stores
+                (37, 4624),     # 256 x 3
+                (1500, 4096),   # 128 x 4
+                (1030, 4624),   # 128 x 5
+                (1030, 4616),   # 128 x 5, 8-byte stores
+                (1030, 6128),   # 128 x 6
+                (300, 8176),    # 256 x 4
+                (4100, 8176),   # 128 x 8
+                (37, 12272),    # 256 x 6
+                (1030, 16368),  # 256 x 8
+                (2050, 16368)]  # 1024 x 2
+
+
+@pytest.mark.parametrize("M,K", ROW_MAPPINGS)
+def test_quantizer_row_mappings(M, K):
+    say(f"quantizer mapping M={M} K={K}")
+    x, _, _ = si.make_inputs((M, K, 1), seed=1300 + K + M, dist="student_t")
+    x[M // 2] = 0
+    q_o, s_o = oracle.quantize_rows(x)
+    q, s = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(q), q_o)
+    assert np.array_equal(host(s).view(np.uint32), s_o.view(np.uint32))
+
+
 @pytest.mark.parametrize("M,K", [(1100, 40000), (600, 24576)])
 def test_quantizer_long_rows_many_blocks(M, K):
     """Rows of a 1024-thread block, more rows than the persistent grid's 512 blocks: each
