@@ -254,8 +254,9 @@ quant_rows_reg(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
     }
 }
 
-// General path: one 256-thread block per row, two passes over the row (the second
-// re-reads it, normally from L2). VEC selects 16-byte loads and 8-byte stores (K % 8 ==
+// General path: a 256-thread block per row (a block takes every G-th row when there are
+// more rows than the grid's G blocks), two passes over the row (the second re-reads it,
+// normally from L2). VEC selects 16-byte loads and 8-byte stores (K % 8 ==
 // 0; v and colmul 16-byte, q 8-byte aligned); a transform is then evaluated on the 8
 // values of a vector in both passes. Otherwise every element is loaded and stored on
 // its own, for any K and any alignment.
@@ -265,85 +266,88 @@ quant_rows_loop(const uint16_t *__restrict__ v, int64_t rows, int64_t K,
                 const float *__restrict__ colmul, int8_t *__restrict__ q,
                 float *__restrict__ scale) {
     constexpr bool PLAIN = ACT == ACT_NONE && !CM;
-    const int64_t row = blockIdx.x;
     const int t = threadIdx.x;
-    const uint16_t *src = v + row * K;
     const int64_t nvec = K >> 3;
-    auto value = [&](int64_t k) {
-        return transform<ACT, CM>(bf16_to_f32(src[k]), CM ? colmul[k] : 1.0f);
-    };
-    // The 8 transformed values of vector vi.
-    auto values8 = [&](int64_t vi, float (&f)[8]) __attribute__((always_inline)) {
-        const uint4 d = reinterpret_cast<const uint4 *>(src)[vi];
-        float c[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
-        if constexpr (CM) {
-            const float4 *c4 = reinterpret_cast<const float4 *>(colmul) + 2 * vi;
-            const float4 lo = c4[0], hi = c4[1];
-            c[0] = lo.x; c[1] = lo.y; c[2] = lo.z; c[3] = lo.w;
-            c[4] = hi.x; c[5] = hi.y; c[6] = hi.z; c[7] = hi.w;
-        }
-        const uint32_t w[4] = {d.x, d.y, d.z, d.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const uint32_t h = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
-            f[e] = transform<ACT, CM>(bf16_to_f32(h), c[e]);
-        }
-    };
-    uint32_t m = 0;
-    if constexpr (VEC && PLAIN) {
-        const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
-        for (int64_t vi = t; vi < nvec; vi += 256)
-            m = max(m, absmax8(s4[vi]));
-    } else if constexpr (VEC) {
-        float fm = 0.0f;
-        for (int64_t vi = t; vi < nvec; vi += 256) {
-            float f[8];
-            values8(vi, f);
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                fm = fmaxf(fm, __builtin_fabsf(f[e]));
-        }
-        m = abs_bits(fm);
-    } else if constexpr (PLAIN) {
-        for (int64_t k = t; k < K; k += 256)
-            m = max(m, (uint32_t)src[k] & 0x7FFFu);
-    } else {
-        for (int64_t k = t; k < K; k += 256)
-            m = max(m, abs_bits(value(k)));
-    }
-    m = wave_max(m);
     __shared__ uint32_t part[4];
-    if ((t & 63) == 0)
-        part[t >> 6] = m;
-    __syncthreads();
-    m = max(max(part[0], part[1]), max(part[2], part[3]));
-    const RowScale rs = PLAIN ? row_scale(m) : row_scale_f(__uint_as_float(m));
-    if (t == 0)
-        scale[row] = rs.scale;
-    int8_t *dst = q + row * K;
-    if constexpr (VEC && PLAIN) {
-        const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
-        uint2 *d2 = reinterpret_cast<uint2 *>(dst);
-        for (int64_t vi = t; vi < nvec; vi += 256)
-            d2[vi] = code8(s4[vi], rs.inv);
-    } else if constexpr (VEC) {
-        uint2 *d2 = reinterpret_cast<uint2 *>(dst);
-        for (int64_t vi = t; vi < nvec; vi += 256) {
-            float f[8];
-            values8(vi, f);
-            uint32_t c[8];
+    // Block b takes rows b, b + G, b + 2G, ... (G = gridDim.x, at most 65536 blocks).
+    for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+        const uint16_t *src = v + row * K;
+        auto value = [&](int64_t k) {
+            return transform<ACT, CM>(bf16_to_f32(src[k]), CM ? colmul[k] : 1.0f);
+        };
+        // The 8 transformed values of vector vi.
+        auto values8 = [&](int64_t vi, float (&f)[8]) __attribute__((always_inline)) {
+            const uint4 d = reinterpret_cast<const uint4 *>(src)[vi];
+            float c[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+            if constexpr (CM) {
+                const float4 *c4 = reinterpret_cast<const float4 *>(colmul) + 2 * vi;
+                const float4 lo = c4[0], hi = c4[1];
+                c[0] = lo.x; c[1] = lo.y; c[2] = lo.z; c[3] = lo.w;
+                c[4] = hi.x; c[5] = hi.y; c[6] = hi.z; c[7] = hi.w;
+            }
+            const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                c[e] = code_f(f[e], rs.inv);
-            d2[vi] = make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
-                                c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t h = (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
+                f[e] = transform<ACT, CM>(bf16_to_f32(h), c[e]);
+            }
+        };
+        uint32_t m = 0;
+        if constexpr (VEC && PLAIN) {
+            const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
+            for (int64_t vi = t; vi < nvec; vi += 256)
+                m = max(m, absmax8(s4[vi]));
+        } else if constexpr (VEC) {
+            float fm = 0.0f;
+            for (int64_t vi = t; vi < nvec; vi += 256) {
+                float f[8];
+                values8(vi, f);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    fm = fmaxf(fm, __builtin_fabsf(f[e]));
+            }
+            m = abs_bits(fm);
+        } else if constexpr (PLAIN) {
+            for (int64_t k = t; k < K; k += 256)
+                m = max(m, (uint32_t)src[k] & 0x7FFFu);
+        } else {
+            for (int64_t k = t; k < K; k += 256)
+                m = max(m, abs_bits(value(k)));
         }
-    } else if constexpr (PLAIN) {
-        for (int64_t k = t; k < K; k += 256)
-            dst[k] = (int8_t)code((uint32_t)src[k], rs.inv);
-    } else {
-        for (int64_t k = t; k < K; k += 256)
-            dst[k] = (int8_t)code_f(value(k), rs.inv);
+        m = wave_max(m);
+        if ((t & 63) == 0)
+            part[t >> 6] = m;
+        __syncthreads();
+        m = max(max(part[0], part[1]), max(part[2], part[3]));
+        __syncthreads();   // part is rewritten for the next row
+        const RowScale rs = PLAIN ? row_scale(m) : row_scale_f(__uint_as_float(m));
+        if (t == 0)
+            scale[row] = rs.scale;
+        int8_t *dst = q + row * K;
+        if constexpr (VEC && PLAIN) {
+            const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
+            uint2 *d2 = reinterpret_cast<uint2 *>(dst);
+            for (int64_t vi = t; vi < nvec; vi += 256)
+                d2[vi] = code8(s4[vi], rs.inv);
+        } else if constexpr (VEC) {
+            uint2 *d2 = reinterpret_cast<uint2 *>(dst);
+            for (int64_t vi = t; vi < nvec; vi += 256) {
+                float f[8];
+                values8(vi, f);
+                uint32_t c[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    c[e] = code_f(f[e], rs.inv);
+                d2[vi] = make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
+                                    c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+            }
+        } else if constexpr (PLAIN) {
+            for (int64_t k = t; k < K; k += 256)
+                dst[k] = (int8_t)code((uint32_t)src[k], rs.inv);
+        } else {
+            for (int64_t k = t; k < K; k += 256)
+                dst[k] = (int8_t)code_f(value(k), rs.inv);
+        }
     }
 }
 
@@ -431,12 +435,13 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             if (nvec <= 8192)
                 return launch_reg<1024, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
     }
+    const unsigned grid = (unsigned)(rows < 65536 ? rows : 65536);
     if (vec)
-        hipLaunchKernelGGL((quant_rows_loop<true, ACT, CM>), dim3((unsigned)rows), dim3(256),
-                           0, s, v, rows, K, colmul, q, scale);
+        hipLaunchKernelGGL((quant_rows_loop<true, ACT, CM>), dim3(grid), dim3(256), 0, s, v,
+                           rows, K, colmul, q, scale);
     else
-        hipLaunchKernelGGL((quant_rows_loop<false, ACT, CM>), dim3((unsigned)rows), dim3(256),
-                           0, s, v, rows, K, colmul, q, scale);
+        hipLaunchKernelGGL((quant_rows_loop<false, ACT, CM>), dim3(grid), dim3(256), 0, s, v,
+                           rows, K, colmul, q, scale);
     return hipGetLastError();
 }
 

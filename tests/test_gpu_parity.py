@@ -127,6 +127,18 @@ def test_quantizer_long_rows_many_blocks(M, K):
     assert np.array_equal(host(s).view(np.uint32), s_o.view(np.uint32))
 
 
+def test_quantizer_more_rows_than_looped_grid():
+    """K % 8 != 0 takes the looped kernel, whose grid stops at 65536 blocks: every block
+    then takes a second row (or more), after the shared row maximum is reused."""
+    M, K = 70001, 5
+    x, _, _ = si.make_inputs((M, K, 1), seed=4242, dist="student_t")
+    x[65536] = 0
+    q_o, s_o = oracle.quantize_rows(x)
+    q, s = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(q), q_o)
+    assert np.array_equal(host(s).view(np.uint32), s_o.view(np.uint32))
+
+
 def test_quantizer_unaligned_pointers():
     K = 256
     x, _, _ = si.make_inputs((20, K + 1, 1), seed=3)
