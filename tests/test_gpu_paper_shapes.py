@@ -2,7 +2,9 @@
 token count M = 4110 (Section 5), through the product path, against the CPU oracle on
 sampled rows and columns (needs an MI355X). M = 4110 fits no tile height, so every
 shape also runs a ragged last row of tiles; K = 53248 (the LLM projection) takes the
-quantizer's two-pass path and the longest accumulation (|acc| up to 8.6e8)."""
+quantizer's 1024-thread rows and the longest accumulation (|acc| up to 8.6e8). The
+N = 4608 shapes also run at 512 and 1024 tokens, where the table picks the 96-channel
+tiles."""
 import numpy as np
 import pytest
 import torch
@@ -30,9 +32,13 @@ def _sample(n, rng, extra=()):
     return np.array(sorted(i for i in base if 0 <= i < n))
 
 
-@pytest.mark.parametrize("name", [p[0] for p in si.PAPER_SHAPES])
-def test_paper_shape_at_in_model_tokens(name):
-    shp = si.paper_shape(name, 4110)
+CASES = [(p[0], 4110) for p in si.PAPER_SHAPES] + [
+    ("attn_out", 512), ("attn_out", 1024), ("ffn_down", 512), ("ffn_down", 1024)]
+
+
+@pytest.mark.parametrize("name,M", CASES)
+def test_paper_shape_at_in_model_tokens(name, M):
+    shp = si.paper_shape(name, M)
     say(f"paper shape {name}: M={shp.M} K={shp.K} N={shp.N} tile="
         f"{w8a8.tile_name(w8a8.select_tile(shp.M, shp.N, shp.K))}")
     x, w, b = si.make_inputs(shp)
