@@ -1118,6 +1118,9 @@ const TileEntry kTiles[] = {
     // 512 or 1024 tokens; 7-8% faster there).
     W8A8_TILE("m128n96k128w4x1s4", 128, 96, 128, 4, 1, 8, 4),
     W8A8_TILE("m256n96k128w4x1s3", 256, 96, 128, 4, 1, 8, 3),
+    // 96 x 256: exactly 256 workgroups at 333 (..384) tokens and N = 16384 (7% faster
+    // there than 128 x 256 on 192).
+    W8A8_TILE("m96n256k128w1x4s3", 96, 256, 128, 1, 4, 8, 3),
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
