@@ -374,35 +374,49 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
                      (reinterpret_cast<uintptr_t>(q) % 8 == 0) &&
                      (reinterpret_cast<uintptr_t>(colmul) % 16 == 0);
     const int64_t nvec = K / 8;
-    // The plain rule past 256 vectors per row: threads per row and vectors per thread
-    // from a sweep of both over rows x K (HIP-graph replays of the quantizer on its own;
-    // the rule keeps every choice within 7% of the sweep's best on the shapes measured).
-    // Fewer rows spread a row over more threads; the vector count per thread is the
-    // smallest that covers the row, so few lanes idle (at K = 4608 a 256 x 4 row leaves
-    // 44% of them idle: 11-24% slower than 128 x 5).
-    if constexpr (PLAIN) {
-        if (vec && nvec > 256 && nvec <= 2048) {
-            if (nvec <= 512) {
+    // Threads per row and vectors per thread past 256 vectors per row, from sweeps of
+    // both over rows x K (HIP-graph replays of the quantizer on its own, the plain rule
+    // and GELU rows). The vector count per thread is the smallest that covers the row,
+    // so few lanes idle (at K = 4608 a 256 x 4 row leaves 44% of them idle: 11-24%
+    // slower than 128 x 5 for the plain rule, 21-28% for GELU rows, which are ALU-bound);
+    // fewer rows spread a row over more threads. Every choice is within 7% of the
+    // sweeps' best on the shapes measured. Transformed rows differ at K <= 4096 (256 x 2
+    // below 4096 rows, 128 x 4 from there, where it beats one wavefront per row), at
+    // K <= 8192 from 4096 rows up (256 x 4) and at K <= 16384 (the 256-thread block
+    // beats 1024-thread rows).
+    if (vec && nvec > 256 && nvec <= 2048) {
+        if (nvec <= 512) {
+            if constexpr (PLAIN) {
                 if (rows < 1024)
                     return launch_reg<512, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                if (rows >= 4096)
+                    return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            } else {
+                // Two vectors per thread keep the 16-byte store pairs of transformed
+                // rows (4 vectors measured 5-8% slower with the multiplier below 4096 rows).
                 if (rows < 4096)
-                    return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-                return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                    return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
             }
-            if (nvec <= 768 && rows < 1024)
-                return launch_reg<256, 3, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            if (nvec <= 640)
-                return launch_reg<128, 5, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            if (nvec <= 768)
-                return launch_reg<128, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            if (nvec <= 1024)
-                return rows < 4096 ? launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s)
-                                   : launch_reg<128, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            if (nvec <= 1536)
-                return launch_reg<256, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            return rows < 2048 ? launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s)
-                               : launch_reg<1024, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         }
+        if (nvec <= 768 && rows < 1024)
+            return launch_reg<256, 3, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 640)
+            return launch_reg<128, 5, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 768)
+            return launch_reg<128, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 1024) {
+            if constexpr (PLAIN)
+                if (rows >= 4096)
+                    return launch_reg<128, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        }
+        if (nvec <= 1536)
+            return launch_reg<256, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if constexpr (PLAIN)
+            if (rows >= 2048)
+                return launch_reg<1024, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        return launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
     }
     if (vec && K > 0) {
         if (nvec <= 64)
@@ -411,19 +425,6 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
             return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 256)
             return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        // Transformed rows with K in (2048, 4096]: a wavefront per row, or the whole
-        // block when there are too few rows to fill the chip with one-wavefront rows
-        // (measured crossover near 4096 rows; its 16-byte store pairs need two vectors
-        // per thread).
-        if (nvec <= 512) {
-            if (rows >= 4096)
-                return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
-            return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        }
-        if (nvec <= 1024)
-            return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        if (nvec <= 2048)
-            return launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
         // Long rows (K up to 65536 for the plain rule, e.g. a 53248-wide projection
         // input; 32768 for transformed rows, whose float32 copy of 8 vectors per thread
         // would not fit 128 VGPRs): a 1024-thread block per row, still read once. The

@@ -95,6 +95,35 @@ def test_colmul_unaligned_multiplier_takes_the_element_path():
     _exact(q, s, q_o, s_o, "unaligned multiplier")
 
 
+# (rows, K) covering each threads-per-row x vectors-per-thread choice for transformed
+# rows past 256 vectors per row, with a ragged last vector.
+TRANSFORM_MAPPINGS = [(1500, 4096),   # 256 x 2
+                      (4100, 3072),   # 128 x 4
+                      (37, 4624),     # 256 x 3
+                      (1030, 4624),   # 128 x 5
+                      (1030, 6128),   # 128 x 6
+                      (300, 8176),    # 256 x 4
+                      (37, 12272),    # 256 x 6
+                      (1030, 16368)]  # 256 x 8
+
+
+@pytest.mark.parametrize("M,K", TRANSFORM_MAPPINGS)
+def test_transformed_row_mappings(M, K):
+    say(f"transformed mapping M={M} K={K}")
+    h, _, _ = si.make_inputs((M, K, 1), seed=1700 + K + M, dist="preact")
+    h[M // 2] = 0
+    cm = np.random.default_rng(K + M).uniform(0.05, 8, K).astype(np.float32)
+    q_o, s_o = oracle.quantize_rows(h, col_mul=cm)
+    q, s = w8a8.quantize_act(dev_bf16(h), col_mul=dev_f32(cm))
+    _exact(q, s, q_o, s_o, f"multiplier M={M} K={K}")
+    q_o, s_o = oracle.quantize_rows(h, act="gelu", col_mul=cm)
+    q, s = w8a8.quantize_act(dev_bf16(h), act="gelu", col_mul=dev_f32(cm))
+    check_gelu_codes(h, host(q), host(s), q_o, s_o, cm, f"gelu*c M={M} K={K}")
+    q_o, s_o = oracle.quantize_rows(h, act="gelu")
+    q, s = w8a8.quantize_act(dev_bf16(h), act="gelu")
+    check_gelu_codes(h, host(q), host(s), q_o, s_o, what=f"gelu M={M} K={K}")
+
+
 # ---------------------------------------------------------------- GELU: within bound
 
 GELU_CASES = [(37, 8), (37, 264), (64, 4096), (9, 16384), (5, 20000), (4, 32768),
