@@ -13,12 +13,14 @@
 // of Section 3 smooths the activations by 1/s[k] and folds s[k] into the weights).
 // Both are evaluated in float32; the row maximum is then taken on float32 values.
 //
-// The kernel is HBM-bound (3 bytes moved per element: 2 read, 1 written). Rows whose
-// K fits the register file are read once with 16-byte loads, kept in VGPRs for the
-// second (quantizing) pass and written with 8-byte stores, by a persistent grid that
-// prefetches the next rows while it finishes the current ones; the row maximum is taken
-// on the bf16 bit patterns (|v| ordered as an unsigned integer, exact for finite values)
-// with a wavefront butterfly and, for rows of several wavefronts, one LDS exchange.
+// The kernel is HBM-bound (3 bytes moved per element: 2 read, 1 written), or ALU-bound
+// with GELU. Rows whose K fits the register file (K <= 65536 for the plain rule) are read
+// once with 16-byte loads, kept in VGPRs for the second (quantizing) pass and written
+// with 16-byte streaming stores where alignment allows (8-byte stores otherwise), by a
+// persistent grid that prefetches the next rows while it finishes the current ones; the
+// row maximum is taken on the bf16 bit patterns (|v| ordered as an unsigned integer,
+// exact for finite values) with a wavefront butterfly and, for rows of several
+// wavefronts, one LDS exchange. Longer rows are read twice by a looped kernel.
 #include "w8a8_internal.hpp"
 #include "quant_math.hpp"
 
