@@ -383,21 +383,35 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
     // slower than 128 x 5 for the plain rule, 21-28% for GELU rows, which are ALU-bound);
     // fewer rows spread a row over more threads. Every choice is within 7% of the
     // sweeps' best on the shapes measured. Transformed rows differ at K <= 4096 (256 x 2
-    // below 4096 rows, 128 x 4 from there, where it beats one wavefront per row), at
-    // K <= 8192 from 4096 rows up (256 x 4) and at K <= 16384 (the 256-thread block
-    // beats 1024-thread rows).
+    // below 4096 rows; from there one wavefront per row up to K = 3584, 3072 without
+    // GELU, and 128 x 4 above), at K <= 8192 from 4096 rows up (256 x 4) and at
+    // K <= 16384 (the 256-thread block beats 1024-thread rows).
     if (vec && nvec > 256 && nvec <= 2048) {
         if (nvec <= 512) {
+            // One wavefront per row with exactly the vectors the row needs.
+            auto wave_row = [&]() {
+                if (nvec <= 320)
+                    return launch_reg<64, 5, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                if (nvec <= 384)
+                    return launch_reg<64, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                if (nvec <= 448)
+                    return launch_reg<64, 7, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            };
             if constexpr (PLAIN) {
                 if (rows < 1024)
                     return launch_reg<512, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
-                if (rows >= 4096)
-                    return launch_reg<64, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                if (rows >= 4096 || nvec <= 384)
+                    return wave_row();
             } else {
                 // Two vectors per thread keep the 16-byte store pairs of transformed
                 // rows (4 vectors measured 5-8% slower with the multiplier below 4096 rows).
                 if (rows < 4096)
                     return launch_reg<256, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+                // Multiplier-only rows are memory-bound: 7 vectors (8-byte stores) measured
+                // 8-9% slower for them than 128 x 4; GELU rows gain up to 8% from it.
+                if (nvec <= (ACT == ACT_GELU ? 448 : 384))
+                    return wave_row();
             }
             return launch_reg<128, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         }

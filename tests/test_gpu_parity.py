@@ -99,7 +99,12 @@ ROW_MAPPINGS = [(37, 4096),     # 512 x 1
                 (4100, 8176),   # 128 x 8
                 (37, 12272),    # 256 x 6
                 (1030, 16368),  # 256 x 8
-                (2050, 16368)]  # 1024 x 2
+                (2050, 16368),  # 1024 x 2
+                (1030, 2568),   # 64 x 5, 8-byte stores
+                (4100, 2560),   # 64 x 5
+                (1030, 3072),   # 64 x 6
+                (4100, 3584),   # 64 x 7
+                (4100, 3568)]   # 64 x 7, ragged last vector
 
 
 @pytest.mark.parametrize("M,K", ROW_MAPPINGS)

@@ -98,7 +98,10 @@ def test_colmul_unaligned_multiplier_takes_the_element_path():
 # (rows, K) covering each threads-per-row x vectors-per-thread choice for transformed
 # rows past 256 vectors per row, with a ragged last vector.
 TRANSFORM_MAPPINGS = [(1500, 4096),   # 256 x 2
-                      (4100, 3072),   # 128 x 4
+                      (4100, 4096),   # 128 x 4
+                      (4100, 2560),   # 64 x 5
+                      (4100, 3072),   # 64 x 6
+                      (4100, 3576),   # 64 x 7
                       (37, 4624),     # 256 x 3
                       (1030, 4624),   # 128 x 5
                       (1030, 6128),   # 128 x 6
