@@ -435,12 +435,20 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
         return launch_reg<256, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
     }
     if (vec && K > 0) {
+        // K <= 2048: below 1024 rows a row takes 128 or 256 threads with one vector each
+        // (8-13% faster than a wavefront per row at K = 1536-2048, 32% with GELU);
+        // from 1024 rows up a wavefront per row with exactly the row's vectors.
         if (nvec <= 64)
             return launch_reg<64, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 128)
-            return launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
-        if (nvec <= 256)
-            return launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return rows < 1024 ? launch_reg<128, 1, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                               : launch_reg<64, 2, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        if (nvec <= 256) {
+            if (rows < 1024)
+                return launch_reg<256, 1, ACT, CM>(v, rows, K, colmul, q, scale, s);
+            return nvec <= 192 ? launch_reg<64, 3, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                               : launch_reg<64, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
+        }
         // Long rows (K up to 65536 for the plain rule, e.g. a 53248-wide projection
         // input; 32768 for transformed rows, whose float32 copy of 8 vectors per thread
         // would not fit 128 VGPRs): a 1024-thread block per row, still read once. The

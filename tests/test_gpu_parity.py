@@ -104,7 +104,13 @@ ROW_MAPPINGS = [(37, 4096),     # 512 x 1
                 (4100, 2560),   # 64 x 5
                 (1030, 3072),   # 64 x 6
                 (4100, 3584),   # 64 x 7
-                (4100, 3568)]   # 64 x 7, ragged last vector
+                (4100, 3568),   # 64 x 7, ragged last vector
+                (300, 1000),    # 128 x 1
+                (1030, 1016),   # 64 x 2
+                (300, 2040),    # 256 x 1
+                (1030, 1536),   # 64 x 3
+                (1030, 1544),   # 64 x 4, 8-byte stores
+                (37, 504)]      # 64 x 1
 
 
 @pytest.mark.parametrize("M,K", ROW_MAPPINGS)

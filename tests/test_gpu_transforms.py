@@ -97,7 +97,10 @@ def test_colmul_unaligned_multiplier_takes_the_element_path():
 
 # (rows, K) covering each threads-per-row x vectors-per-thread choice for transformed
 # rows past 256 vectors per row, with a ragged last vector.
-TRANSFORM_MAPPINGS = [(1500, 4096),   # 256 x 2
+TRANSFORM_MAPPINGS = [(300, 1000),    # 128 x 1
+                      (300, 2040),    # 256 x 1
+                      (1030, 1536),   # 64 x 3
+                      (1500, 4096),   # 256 x 2
                       (4100, 4096),   # 128 x 4
                       (4100, 2560),   # 64 x 5
                       (4100, 3072),   # 64 x 6
