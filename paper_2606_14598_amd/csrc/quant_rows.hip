@@ -427,6 +427,11 @@ hipError_t launch_rows(const uint16_t *v, int64_t rows, int64_t K, const float *
                     return launch_reg<128, 8, ACT, CM>(v, rows, K, colmul, q, scale, s);
             return launch_reg<256, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         }
+        // Few long rows (K > 8192 below 256 rows): 512 threads per row, 5-9% faster
+        // than the 256-thread block.
+        if (rows < 256)
+            return nvec <= 1536 ? launch_reg<512, 3, ACT, CM>(v, rows, K, colmul, q, scale, s)
+                                : launch_reg<512, 4, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if (nvec <= 1536)
             return launch_reg<256, 6, ACT, CM>(v, rows, K, colmul, q, scale, s);
         if constexpr (PLAIN)

@@ -97,7 +97,7 @@ ROW_MAPPINGS = [(37, 4096),     # 512 x 1
                 (1030, 6128),   # 128 x 6
                 (300, 8176),    # 256 x 4
                 (4100, 8176),   # 128 x 8
-                (37, 12272),    # 256 x 6
+                (300, 12272),   # 256 x 6
                 (1030, 16368),  # 256 x 8
                 (2050, 16368),  # 1024 x 2
                 (1030, 2568),   # 64 x 5, 8-byte stores
@@ -110,7 +110,9 @@ ROW_MAPPINGS = [(37, 4096),     # 512 x 1
                 (300, 2040),    # 256 x 1
                 (1030, 1536),   # 64 x 3
                 (1030, 1544),   # 64 x 4, 8-byte stores
-                (37, 504)]      # 64 x 1
+                (37, 504),      # 64 x 1
+                (200, 12272),   # 512 x 3
+                (255, 16368)]   # 512 x 4
 
 
 @pytest.mark.parametrize("M,K", ROW_MAPPINGS)

@@ -109,7 +109,8 @@ TRANSFORM_MAPPINGS = [(300, 1000),    # 128 x 1
                       (1030, 4624),   # 128 x 5
                       (1030, 6128),   # 128 x 6
                       (300, 8176),    # 256 x 4
-                      (37, 12272),    # 256 x 6
+                      (37, 12272),    # 512 x 3
+                      (300, 12272),   # 256 x 6
                       (1030, 16368)]  # 256 x 8
 
 
