@@ -104,6 +104,12 @@ w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scal
 
 size_t w8a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
+/* 1 if w8a8_linear runs quantizer and GEMM as one launch for this shape when x and wq
+ * are 16-byte aligned (the few-token path above; its token block, codes and scales,
+ * must fit the workgroup's LDS beside the tile's own), else 0. A pure host query: it
+ * launches nothing and needs no device. */
+int w8a8_linear_one_launch(int64_t M, int64_t N, int64_t K);
+
 /* Debug: the raw int32 accumulator acc [M,N] = Xq Wq^T, with no epilogue. It is the
  * exactness check the paper runs against a library integer matmul (Section 5,
  * "The kernel is exact and the GEMMs are compute-bound"). */

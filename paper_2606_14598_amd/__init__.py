@@ -31,7 +31,7 @@ import torch
 __all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
            "col_absmax", "smooth_factors", "ACTS",
            "tile_count", "tile_name", "select_tile", "default_tile", "gemm_workspace_bytes",
-           "linear_workspace_bytes", "library_path", "load_library", "W8A8Error",
+           "linear_workspace_bytes", "linear_one_launch", "library_path", "load_library", "W8A8Error",
            "MAX_K", "version", "mfma_ceiling", "mfma_ceiling_ops"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -76,6 +76,7 @@ def load_library():
         "w8a8_gemm_workspace_bytes_ex": ([I64, I64, I64, INT], SZ),
         "w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P, SZ, P], INT),
         "w8a8_linear_workspace_bytes": ([I64, I64, I64], SZ),
+        "w8a8_linear_one_launch": ([I64, I64, I64], INT),
         "w8a8_gemm_acc_i32": ([P, P, P, I64, I64, I64, P], INT),
         "w8a8_gemm_acc_i32_ex": ([P, P, P, I64, I64, I64, INT, P], INT),
         "w8a8_tile_count": ([], INT),
@@ -123,6 +124,16 @@ def _check(t: torch.Tensor, dtype: torch.dtype, ndim: int, name: str):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _check_out(t, dtype: torch.dtype, shape: tuple, device, name: str = "out"):
+    """A caller-provided output: the dtype, shape and device the kernels will write,
+    contiguous (they write shape[0] * shape[1] elements from its first element)."""
+    _check(t, dtype, len(shape), name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.device != torch.device(device):
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
 def _same_device(*ts):
     devs = {t.device for t in ts if t is not None}
     if len(devs) > 1:
@@ -159,6 +170,12 @@ def gemm_workspace_bytes(M: int, N: int, K: int, tile: int = -1) -> int:
 
 def linear_workspace_bytes(M: int, N: int, K: int) -> int:
     return int(load_library().w8a8_linear_workspace_bytes(M, N, K))
+
+
+def linear_one_launch(M: int, N: int, K: int) -> bool:
+    """Whether linear() runs quantizer and GEMM as one launch for this shape (16-byte
+    aligned x and wq): a host query, no device needed."""
+    return bool(load_library().w8a8_linear_one_launch(M, N, K))
 
 
 ACTS = {"none": 0, "gelu": 1}
@@ -249,6 +266,10 @@ def _workspace(nbytes: int, device, workspace):
     if nbytes == 0:
         return None
     if workspace is not None:
+        if not isinstance(workspace, torch.Tensor) or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous torch.Tensor")
+        if workspace.device != torch.device(device):
+            raise ValueError(f"workspace is on {workspace.device}, expected {device}")
         if workspace.numel() * workspace.element_size() < nbytes:
             raise ValueError(f"workspace needs {nbytes} bytes")
         return workspace
@@ -270,9 +291,10 @@ def gemm(xq, x_scale, wq, w_scale, bias=None, *, tile: int = -1, out=None,
     if wq.shape[1] != K or x_scale.shape[0] != M or w_scale.shape[0] != N or (
             bias is not None and bias.shape[0] != N):
         raise ValueError("shape mismatch")
+    if out is not None:
+        _check_out(out, torch.bfloat16, (M, N), xq.device)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
                                                 device=xq.device)
-    _check(y, torch.bfloat16, 2, "out")
     ws = _workspace(gemm_workspace_bytes(M, N, K, tile), xq.device, workspace)
     nws = 0 if ws is None else ws.numel() * ws.element_size()
     with torch.cuda.device(xq.device):
@@ -302,6 +324,8 @@ def linear(x, wq, w_scale, bias=None, *, act: str = "none", col_mul=None, out=No
     if wq.shape[1] != K or w_scale.shape[0] != N or (bias is not None and bias.shape[0] != N):
         raise ValueError("shape mismatch")
     cm = _col_mul(col_mul, K, x.device)
+    if out is not None:
+        _check_out(out, torch.bfloat16, (M, N), x.device)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16,
                                                 device=x.device)
     if M == 0 or N == 0:
@@ -322,9 +346,10 @@ def gemm_acc_i32(xq, wq, *, tile: int = -1, out=None):
     N = wq.shape[0]
     if wq.shape[1] != K:
         raise ValueError("shape mismatch")
+    if out is not None:
+        _check_out(out, torch.int32, (M, N), xq.device)
     acc = out if out is not None else torch.empty((M, N), dtype=torch.int32,
                                                   device=xq.device)
-    _check(acc, torch.int32, 2, "out")
     with torch.cuda.device(xq.device):
         _call("w8a8_gemm_acc_i32_ex", _ptr(xq), _ptr(wq), _ptr(acc), M, N, K, int(tile),
               _stream(xq.device))

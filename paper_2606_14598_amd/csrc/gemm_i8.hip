@@ -1217,19 +1217,29 @@ size_t tile_workspace_bytes(int id, int64_t M, int64_t N, int64_t K) {
     return splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * sizeof(int32_t) : 0;
 }
 
+// LDS of one workgroup on gfx950.
+constexpr int64_t kLdsPerWorkgroup = 160 * 1024;
+
 // The small fused linear (see gemm_i8_skinny_kernel, QX): the chosen tile streams the
 // weight, K % 16 == 0 with 16-byte aligned operands, a token block's codes and scales fit
-// in 48 KB of LDS, and the repeated reads of X (once per channel block) total at most
-// 16 MB.
+// in 48 KB of LDS and, with the tile's static LDS (its cross-wavefront reduction array),
+// in the workgroup's 160 KB, and the repeated reads of X (once per channel block) total
+// at most 16 MB.
 bool linear_small_applies(int64_t M, int64_t N, int64_t K, const void *x, const void *wq) {
-    if (M <= 0 || N <= 0 || K <= 0 || K % 16 != 0 ||
-        reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(wq) % 16 != 0)
+    if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(wq) % 16 != 0)
+        return false;
+    return linear_small_shape(M, N, K);
+}
+
+bool linear_small_shape(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K <= 0 || K % 16 != 0)
         return false;
     const TileInfo &t = kTiles[select_tile(M, N, K)].info;
     if (!t.streaming)
         return false;
     const int64_t rows = M < t.tm ? M : t.tm;
-    if (rows * (K + 16) + rows * 4 > 48 * 1024)
+    const int64_t dyn = rows * (K + 16) + rows * 4;
+    if (dyn > 48 * 1024 || dyn + t.lds_bytes > kLdsPerWorkgroup)
         return false;
     // The quantization is a serial chain per wavefront (one row per wavefront, its
     // 16-byte vectors strided over the lanes, two passes): past 7 vectors per lane it

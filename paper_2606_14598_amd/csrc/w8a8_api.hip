@@ -244,6 +244,13 @@ w8a8_status w8a8_gemm_acc_i32(const int8_t *xq, const int8_t *wq, int32_t *acc,
     return w8a8_gemm_acc_i32_ex(xq, wq, acc, M, N, K, -1, stream);
 }
 
+int w8a8_linear_one_launch(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K < 0 || K > W8A8_MAX_K || !product_ok(M, K) ||
+        !product_ok(N, K) || !product_ok(M, N))
+        return 0;
+    return linear_small_shape(M, N, K) ? 1 : 0;
+}
+
 int w8a8_tile_count(void) { return tile_count(); }
 
 const char *w8a8_tile_name(int tile_id) {

@@ -64,6 +64,8 @@ hipError_t launch_gemm(int id, Epilogue epi, bool vec, const GemmArgs &a, void *
 // is a weight-streaming one and whose token blocks are small enough to be quantized by
 // every workgroup that uses them (plain rule only: no transform, no multiplier).
 bool linear_small_applies(int64_t M, int64_t N, int64_t K, const void *x, const void *wq);
+// The shape part of that rule (operands assumed 16-byte aligned).
+bool linear_small_shape(int64_t M, int64_t N, int64_t K);
 hipError_t launch_linear_small(const uint16_t *x, const int8_t *wq, const float *sw,
                                const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
                                int64_t K, hipStream_t stream);

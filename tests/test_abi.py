@@ -210,3 +210,76 @@ def test_mfma_ceiling_validation(lib):
     # ops of one launch: 256 workgroups x 4 wavefronts x 8 K-steps x 10 MFMAs x 65536 ops
     assert lib.w8a8_mfma_ceiling_ops(3) == 256 * 4 * 3 * 8 * 10 * 65536
     assert lib.w8a8_mfma_ceiling_ops(0) == -1
+
+
+def _skinny_static_lds(name: str) -> int:
+    """Static LDS of a weight-streaming tile, from its name skinny_m<M>n<C>w<NW>: the
+    cross-wavefront reduction array holds NW x (C/16) x (M/16) x 64 lanes x 16 bytes."""
+    m = re.match(r"skinny_m(\d+)n(\d+)w(\d+)$", name)
+    assert m, name
+    tm, tn, nw = (int(g) for g in m.groups())
+    return nw * (tn // 16) * (tm // 16) * 64 * 16
+
+
+def test_one_launch_linear_fits_the_workgroup_lds(lib):
+    """Wherever w8a8_linear takes the one-launch path, the token block's codes (rows of
+    K + 16 bytes) and scales plus the tile's static LDS fit gfx950's 160 KiB."""
+    budget = 160 * 1024
+    seen = 0
+    for M in list(range(1, 129)):
+        for K in (16, 256, 512, 768, 1024, 2048, 3136, 4096):
+            for N in (64, 520, 4096, 16384):
+                if not lib.w8a8_linear_one_launch(M, N, K):
+                    continue
+                seen += 1
+                name = lib.w8a8_tile_name(lib.w8a8_select_tile(M, N, K)).decode()
+                tm = int(re.match(r"skinny_m(\d+)", name).group(1))
+                rows = min(M, tm)
+                dyn = rows * (K + 16) + rows * 4
+                assert dyn <= 48 * 1024, (M, N, K, name)
+                assert dyn + _skinny_static_lds(name) <= budget, (M, N, K, name)
+    assert seen > 100
+    # shapes that once passed the dynamic check alone but overflow the total
+    assert not lib.w8a8_linear_one_launch(64, 4096, 512)
+    assert not lib.w8a8_linear_one_launch(48, 4096, 768)
+    # and shapes that do take the path
+    assert lib.w8a8_linear_one_launch(64, 128, 256)
+    assert lib.w8a8_linear_one_launch(1, 4096, 3136)
+    assert not lib.w8a8_linear_one_launch(0, 4096, 3136)
+    assert not lib.w8a8_linear_one_launch(16, 4096, 264)     # K % 16 != 0
+
+
+def test_python_binding_checks_out_and_workspace():
+    """A caller's out tensor must have the dtype, shape and device the kernels write: an
+    undersized or mistyped out is rejected before any launch (fake tensors stand in for
+    device memory, so this runs without a GPU)."""
+    import torch
+    from torch._subclasses.fake_tensor import FakeTensorMode
+    with FakeTensorMode():
+        M, K, N = 33, 256, 64
+        x = torch.empty(M, K, dtype=torch.bfloat16, device="cuda")
+        wq = torch.empty(N, K, dtype=torch.int8, device="cuda")
+        sw = torch.empty(N, dtype=torch.float32, device="cuda")
+        xq = torch.empty(M, K, dtype=torch.int8, device="cuda")
+        sx = torch.empty(M, dtype=torch.float32, device="cuda")
+        bad_outs = [torch.empty(M, N - 1, dtype=torch.bfloat16, device="cuda"),
+                    torch.empty(M - 1, N, dtype=torch.bfloat16, device="cuda"),
+                    torch.empty(M * N, dtype=torch.bfloat16, device="cuda"),
+                    torch.empty(M, N, dtype=torch.float32, device="cuda"),
+                    torch.empty(N, M, dtype=torch.bfloat16, device="cuda").t(),
+                    torch.empty(M, N, dtype=torch.bfloat16, device="cpu")]
+        for out in bad_outs:
+            with pytest.raises((ValueError, TypeError)):
+                w8a8.linear(x, wq, sw, out=out)
+            with pytest.raises((ValueError, TypeError)):
+                w8a8.gemm(xq, sx, wq, sw, out=out)
+        for out in (torch.empty(M, N - 1, dtype=torch.int32, device="cuda"),
+                    torch.empty(M, N, dtype=torch.bfloat16, device="cuda")):
+            with pytest.raises((ValueError, TypeError)):
+                w8a8.gemm_acc_i32(xq, wq, out=out)
+        need = w8a8.linear_workspace_bytes(M, N, K)
+        with pytest.raises(ValueError):
+            w8a8.linear(x, wq, sw, workspace=torch.empty(need - 1, dtype=torch.uint8,
+                                                          device="cuda"))
+        with pytest.raises(ValueError):
+            w8a8.linear(x, wq, sw, workspace=torch.empty(need, dtype=torch.uint8))
