@@ -56,7 +56,8 @@ enum {
     W8A8_ERR_K_OVERFLOW = 3,  /* K > W8A8_MAX_K: 127*127*K would not fit int32 */
     W8A8_ERR_HIP = 4,         /* HIP reported an error for a launch */
     W8A8_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query returns */
-    W8A8_ERR_ARG = 6          /* another invalid argument (e.g. unknown tile id) */
+    W8A8_ERR_ARG = 6,         /* another invalid argument (e.g. unknown tile id) */
+    W8A8_ERR_SCRATCH = 7      /* w8a8_linear_noalloc: the problem exceeds its scratch */
 };
 
 /* Largest K for which |acc| <= 127 * 127 * K fits int32. */
@@ -103,6 +104,24 @@ w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scal
                         void *stream);
 
 size_t w8a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/* For callers that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): w8a8_linear_ex without a workspace argument. The
+ * workspace lives in a file-scope device array of W8A8_NOALLOC_SCRATCH_BYTES that each
+ * device holds from the library's load until the process ends; the call itself allocates
+ * nothing (no hipMalloc, no allocating library routine). Its first call on a device
+ * looks up that device's array once (hipGetSymbolAddress), so make it outside graph
+ * capture. Problems whose w8a8_linear_workspace_bytes(M,N,K) exceeds the array return
+ * W8A8_ERR_SCRATCH before anything is launched (128 MiB holds, e.g., Xq of 4608 tokens
+ * at K = 16384). Every call on a device shares that device's array and leaves its
+ * contents behind (nothing in it needs to start at zero): calls that overlap on one
+ * device, on different streams or from different threads, race and give undefined
+ * results. Arguments and results are those of w8a8_linear_ex. */
+#define W8A8_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+w8a8_status w8a8_linear_noalloc(const uint16_t *x, int act, const float *col_mul,
+                                const int8_t *wq, const float *w_scale,
+                                const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                                int64_t K, void *stream);
 
 /* 1 if w8a8_linear runs quantizer and GEMM as one launch for this shape when x and wq
  * are 16-byte aligned (the few-token path above; its token block, codes and scales,

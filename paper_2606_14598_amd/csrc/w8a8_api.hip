@@ -3,6 +3,8 @@
 #include "../../include/w8a8.h"
 #include "w8a8_internal.hpp"
 
+#include <mutex>
+
 namespace {
 
 using namespace w8a8;
@@ -75,6 +77,40 @@ w8a8_status run_gemm(const int8_t *xq, const float *sx, const int8_t *wq, const 
     a.K = K;
     const bool vec = (K % 16 == 0) && aligned16(xq) && aligned16(wq);
     return from_hip(launch_gemm(id, epi, vec, a, ws, ws_bytes, s));
+}
+
+// Scratch of w8a8_linear_noalloc: Xq, sx and the GEMM's split-K partials, laid out as
+// in w8a8_linear's workspace. Each device holds its own copy from the time the library's
+// code object is loaded onto it until the process ends. In host code `scratch` names a
+// host-side shadow, not device memory: kernels get the address hipGetSymbolAddress
+// returns for the current device, never the name itself.
+static __device__ __align__(256) char scratch[W8A8_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, looked up once per device (with that device
+// current) and kept.
+hipError_t scratch_for_current_device(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        if (!p || reinterpret_cast<uintptr_t>(p) % kAlign != 0)
+            return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace
@@ -219,6 +255,32 @@ w8a8_status w8a8_linear(const uint16_t *x, const int8_t *wq, const float *w_scal
                           workspace, workspace_bytes, stream);
 }
 
+w8a8_status w8a8_linear_noalloc(const uint16_t *x, int act, const float *col_mul,
+                                const int8_t *wq, const float *w_scale,
+                                const uint16_t *bias, uint16_t *y, int64_t M, int64_t N,
+                                int64_t K, void *stream) {
+    // The same checks as w8a8_linear_ex, then the size limit, all before any HIP call.
+    if (!act_ok(act))
+        return W8A8_ERR_ARG;
+    if (M < 0 || N < 0 || K < 0 || !product_ok(M, K) || !product_ok(N, K) ||
+        !product_ok(M, N))
+        return W8A8_ERR_SHAPE;
+    if (K > W8A8_MAX_K)
+        return W8A8_ERR_K_OVERFLOW;
+    if (M == 0 || N == 0)
+        return W8A8_OK;
+    if (!y || !w_scale || (K > 0 && (!x || !wq)))
+        return W8A8_ERR_NULL;
+    const size_t need = w8a8_linear_workspace_bytes(M, N, K);
+    if (need > W8A8_NOALLOC_SCRATCH_BYTES)
+        return W8A8_ERR_SCRATCH;
+    void *ptr = nullptr;
+    if (scratch_for_current_device(&ptr) != hipSuccess)
+        return W8A8_ERR_HIP;
+    return w8a8_linear_ex(x, act, col_mul, wq, w_scale, bias, y, M, N, K, ptr,
+                          W8A8_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 w8a8_status w8a8_gemm_acc_i32_ex(const int8_t *xq, const int8_t *wq, int32_t *acc,
                                  int64_t M, int64_t N, int64_t K, int tile_id,
                                  void *stream) {
@@ -279,6 +341,8 @@ const char *w8a8_status_string(w8a8_status status) {
     case W8A8_ERR_HIP: return "HIP launch error";
     case W8A8_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     case W8A8_ERR_ARG: return "invalid argument";
+    case W8A8_ERR_SCRATCH:
+        return "problem needs more than the no-allocation entry point's scratch";
     default: return "unknown status";
     }
 }

@@ -50,7 +50,7 @@ def test_no_internal_symbols_exported():
 
 
 def test_status_strings(lib):
-    for st in range(7):
+    for st in range(8):
         assert lib.w8a8_status_string(st)
     assert lib.w8a8_status_string(99) == b"unknown status"
 
@@ -283,3 +283,21 @@ def test_python_binding_checks_out_and_workspace():
                                                           device="cuda"))
         with pytest.raises(ValueError):
             w8a8.linear(x, wq, sw, workspace=torch.empty(need, dtype=torch.uint8))
+
+
+def test_noalloc_validation_before_any_device_call(lib):
+    """w8a8_linear_noalloc validates like w8a8_linear_ex and rejects problems beyond its
+    128 MiB scratch before it looks up the device array (so this runs without a GPU)."""
+    P = ctypes.c_void_p
+    fake = P(256)
+    f = lib.w8a8_linear_noalloc
+    f.argtypes = [P, ctypes.c_int, P, P, P, P, P, ctypes.c_int64, ctypes.c_int64,
+                  ctypes.c_int64, P]
+    f.restype = ctypes.c_int
+    assert f(fake, 0, None, fake, fake, None, fake, 8192, 64, 16384, None) == 7
+    assert lib.w8a8_status_string(7)
+    assert f(fake, 5, None, fake, fake, None, fake, 4, 8, 16, None) == ERR_ARG
+    assert f(fake, 0, None, fake, fake, None, fake, -4, 8, 16, None) == ERR_SHAPE
+    assert f(fake, 0, None, fake, fake, None, fake, 4, 8, w8a8.MAX_K + 1, None) == ERR_K
+    assert f(fake, 0, None, fake, None, None, fake, 4, 8, 16, None) == ERR_NULL
+    assert f(None, 0, None, None, None, None, None, 0, 8, 16, None) == OK
