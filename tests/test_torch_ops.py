@@ -1,11 +1,14 @@
 """The torch.library registration: schemas and fake (meta) implementations on the CPU,
 real calls, opcheck and torch.compile without graph breaks on the GPU."""
+import numpy as np
 import pytest
 import torch
 from torch._subclasses.fake_tensor import FakeTensorMode
 
+import oracle
 import paper_2606_14598_amd as w8a8
 import paper_2606_14598_amd.torch_ops as ops
+from _gelu_checks import check_gelu_linear_against_oracle_chain
 
 
 def test_ops_are_registered():
@@ -50,7 +53,25 @@ def test_module_and_compile_without_graph_breaks():
     explained = torch._dynamo.explain(block)(x)
     assert explained.graph_break_count == 0, explained.break_reasons
     compiled = torch.compile(block, fullgraph=True, backend="aot_eager")
-    assert torch.equal(compiled(x), eager)
+    got = compiled(x)
+    assert torch.equal(got, eager)
+    # ... and the module path against the oracle's chain, which never sees a GPU
+    # result: both weights quantized by the oracle, the first linear exactly, the
+    # GELU-quantized second linear within the GELU bound, and the compiled output equal
+    # to that second linear plus 1.0 rounded once to bf16 by the oracle's own rounding.
+    bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    wq1, sw1 = oracle.quantize_rows(bits(lin1.weight))
+    wq2, sw2 = oracle.quantize_rows(bits(lin2.weight))
+    assert np.array_equal(m1.wq.cpu().numpy(), wq1) and np.array_equal(m2.wq.cpu().numpy(), wq2)
+    h_o, _, _, _ = oracle.linear(bits(x).reshape(-1, 1024), wq1, sw1, bits(lin1.bias))
+    assert np.array_equal(bits(h).reshape(-1, 2048), h_o)
+    y2 = w8a8.linear(h, m2.wq, m2.w_scale, m2.bias, act="gelu").reshape(-1, 512)
+    hq, hs = w8a8.quantize_act(h.reshape(-1, 2048), act="gelu")
+    check_gelu_linear_against_oracle_chain(h_o, wq2, sw2, bits(lin2.bias), bits(y2),
+                                           hq.cpu().numpy(), hs.cpu().numpy(),
+                                           "module's second linear")
+    plus1 = oracle.f32_to_bf16(oracle.bf16_to_f32(bits(y2)) + np.float32(1.0))
+    assert np.array_equal(bits(got).reshape(-1), plus1)
 
 
 @pytest.mark.gpu
