@@ -659,27 +659,44 @@ def all_shapes(args):
                    "speedup_linear_vs_bf16": round(bf / lin, 3),
                    "timing": "median of 5 repeats"}
             if M <= 333:
-                # cold: a 512 MB scrub write before every call, so the 256 MB MALL cannot
-                # serve the weight; each call timed alone with HIP events
-                scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-                cold = {"lin": [], "gem": [], "bf": []}
                 fns = {"lin": lambda: w8a8.linear(xd, wq, sw, bd, out=y, workspace=ws),
                        "gem": lambda: w8a8.gemm(xq, sx, wq, sw, bd, out=y, workspace=gws),
                        "bf": lambda: F.linear(xd, wd, bd)}
+                # Cold (read scrub): each call preceded by a 1 GiB read of another buffer, so
+                # the 256 MB MALL holds none of the operands and no dirty lines; in one HIP
+                # graph of 10 (scrub, call) pairs, minus the graph of the 10 scrubs alone.
+                # This is the call's own time plus one kernel boundary, with no host
+                # launch or event-timing floor.
+                scrub = torch.zeros((1 << 29) // 4096, 4096, dtype=torch.bfloat16, device=dev)
+                amax = torch.empty(4096, dtype=torch.float32, device=dev)
+                rs = lambda: w8a8.col_absmax(scrub, out=amax)
+                base = graph_ms(rs, iters=10, warm_ms=5.0)
+                cold = {k: graph_ms(lambda f=f: (rs(), f()), iters=10, warm_ms=5.0) - base
+                        for k, f in fns.items()}
+                rec["cold_read_us"] = {"linear": round(cold["lin"] * 1e3, 2),
+                                       "gemm": round(cold["gem"] * 1e3, 2),
+                                       "bf16_linear": round(cold["bf"] * 1e3, 2)}
+                rec["cold_read_gemm_hbm_GB_s"] = round(gb / cold["gem"] / 1e6, 1)
+                # Cold (write scrub, the earlier method): a 512 MB scrub write before every
+                # call, each call timed alone with HIP events. The scrub leaves the MALL
+                # full of dirty lines that the call then writes back, and single-call event
+                # timing adds ~6 us of launch floor.
+                wscrub = scrub.view(torch.uint8)[: 512 << 20]
+                coldw = {"lin": [], "gem": [], "bf": []}
                 for _ in range(10):
                     for k, f in fns.items():
-                        scrub.fill_(1)
+                        wscrub.fill_(1)
                         st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                         st.record()
                         f()
                         en.record()
                         torch.cuda.synchronize()
-                        cold[k].append(st.elapsed_time(en))
-                cl, cg, cb = (sorted(cold[k])[5] for k in ("lin", "gem", "bf"))
-                rec["cold_us"] = {"linear": round(cl * 1e3, 2), "gemm": round(cg * 1e3, 2),
-                                  "bf16_linear": round(cb * 1e3, 2)}
-                rec["cold_gemm_hbm_GB_s"] = round(gb / cg / 1e6, 1)
-                del scrub
+                        coldw[k].append(st.elapsed_time(en))
+                cl, cg, cb = (sorted(coldw[k])[5] for k in ("lin", "gem", "bf"))
+                rec["cold_write_us"] = {"linear": round(cl * 1e3, 2), "gemm": round(cg * 1e3, 2),
+                                        "bf16_linear": round(cb * 1e3, 2)}
+                rec["cold_write_gemm_hbm_GB_s"] = round(gb / cg / 1e6, 1)
+                del scrub, wscrub
             print(json.dumps(rec), flush=True)
             del xd, wd, bd, wq, sw, xq, sx, y, ws, gws
 
