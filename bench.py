@@ -29,6 +29,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extr
        python bench.py --all-shapes           (every workload shape, one JSON line each)
        python bench.py --recipe               (GELU / SmoothQuant quantizer, shared X)
        python bench.py --paper-shapes         (the paper's five shapes, tuned vs untuned)
+       python bench.py --gemm-study           (headline GEMMs on other operand bits, hipBLASLt int8)
        python bench.py --copy-calibration     (a known-size copy for counter scaling)
 """
 from __future__ import annotations
@@ -874,6 +875,61 @@ def paper_shapes(args):
                           "tuned_tops": rng("tops", "tuned")}), flush=True)
 
 
+def gemm_study(args):
+    """The four DiT-block GEMMs at M = 4608 (the headline's dominant kernels), HIP-graph
+    replays: the fused GEMM on the workload's codes, on all-zero codes, on constant codes
+    and on uniform random codes in [-127, 127] (the same launch, only the operand bits
+    change, so the difference is what the matrix cores' switching costs); hipBLASLt's
+    int8 GEMM (torch._int_mm, int32 out, no epilogue) and bf16 F.linear on the same
+    shapes. One JSON line per shape."""
+    import torch
+    import torch.nn.functional as F
+    import paper_2606_14598_amd as w8a8
+    import synth_inputs as si
+    dev = torch.device("cuda:0")
+    for name in HEADLINE_NAMES:
+        shp = si.workload(HEADLINE_CONFIG, name)
+        M, N, K = shp.M, shp.N, shp.K
+        x, w, b = si.make_inputs(shp)
+        xd, wd, bd = dev_bf16(x, dev), dev_bf16(w, dev), dev_bf16(b, dev)
+        wq, sw = w8a8.quantize_weight(wd)
+        xq, sx = w8a8.quantize_act(xd)
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        g = torch.Generator(device=dev).manual_seed(shp.seed)
+        codes = {
+            "workload": (xq, wq),
+            "zeros": (torch.zeros_like(xq), torch.zeros_like(wq)),
+            "ones": (torch.ones_like(xq), torch.ones_like(wq)),
+            "uniform_random": (
+                torch.randint(-127, 128, xq.shape, device=dev, dtype=torch.int8, generator=g),
+                torch.randint(-127, 128, wq.shape, device=dev, dtype=torch.int8, generator=g)),
+        }
+        ops = gemm_ops(M, N, K)
+        rec = {"what": "gemm_study", "shape": name, "M": M, "K": K, "N": N,
+               "tile": w8a8.tile_name(w8a8.select_tile(M, N, K)),
+               "mean_abs_code": {"x": round(float(xq.float().abs().mean()), 2),
+                                 "w": round(float(wq.float().abs().mean()), 2)}}
+        us, tops = {}, {}
+        for k, (a, bq) in codes.items():
+            t = graph_ms(lambda: w8a8.gemm(a, sx, bq, sw, bd, out=y), iters=10, warm_ms=40.0)
+            us[k], tops[k] = round(t * 1e3, 2), round(ops / t / 1e9, 1)
+        wt = wq.t()
+        try:
+            torch._int_mm(xq, wt)
+            t = graph_ms(lambda: torch._int_mm(xq, wt), iters=10, warm_ms=40.0)
+            us["hipblaslt_int8_int32_out"], tops["hipblaslt_int8_int32_out"] = (
+                round(t * 1e3, 2), round(ops / t / 1e9, 1))
+        except Exception as e:  # noqa: BLE001
+            rec["hipblaslt_int8"] = f"unavailable: {type(e).__name__}"
+        t = graph_ms(lambda: F.linear(xd, wd, bd), iters=10, warm_ms=40.0)
+        us["bf16_linear"], tops["bf16_linear"] = round(t * 1e3, 2), round(ops / t / 1e9, 1)
+        rec["us"], rec["tops"] = us, tops
+        rec["frac_of_peak"] = {k: round(v / PEAK_INT8_TOPS, 4) for k, v in tops.items()}
+        print(json.dumps(rec), flush=True)
+        del xd, wd, bd, wq, sw, xq, sx, y, codes
+        torch.cuda.empty_cache()
+
+
 def copy_calibration():
     """A plain device copy of known size (for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE)."""
     import torch
@@ -903,6 +959,9 @@ def main():
                     help="time every workload shape (one JSON line each)")
     ap.add_argument("--paper-shapes", action="store_true",
                     help="the paper's five model shapes over M = 512..16384, tuned vs untuned")
+    ap.add_argument("--gemm-study", action="store_true",
+                    help="the headline GEMMs on workload / zero / constant / random codes, "
+                         "beside hipBLASLt int8 and bf16")
     ap.add_argument("--recipe", action="store_true",
                     help="time GELU / SmoothQuant in the quantizer and shared quantization")
     args = ap.parse_args()
@@ -922,6 +981,9 @@ def main():
         return
     if args.recipe:
         recipe(args)
+        return
+    if args.gemm_study:
+        gemm_study(args)
         return
     if args.paper_shapes:
         paper_shapes(args)
