@@ -678,6 +678,16 @@ def all_shapes(args):
                                        "gemm": round(cold["gem"] * 1e3, 2),
                                        "bf16_linear": round(cold["bf"] * 1e3, 2)}
                 rec["cold_read_gemm_hbm_GB_s"] = round(gb / cold["gem"] / 1e6, 1)
+                # The achievable floor: a plain streaming read of Wq's own bytes, timed
+                # cold the same way (w8a8_read_ceiling). A weight-streaming GEMM reads
+                # those bytes once, so this is the rate HBM actually gives it.
+                if wq.numel() % (16 * w8a8.READ_BLOCKS) == 0:
+                    rsum = torch.empty(w8a8.READ_BLOCKS, dtype=torch.int32, device=dev)
+                    rd = lambda: w8a8.read_ceiling(wq, out=rsum)
+                    floor = graph_ms(lambda: (rs(), rd()), iters=10, warm_ms=5.0) - base
+                    rec["cold_read_floor_us"] = round(floor * 1e3, 2)
+                    rec["cold_read_floor_GB_s"] = round(wq.numel() / floor / 1e6, 1)
+                    rec["gemm_cold_frac_of_read_floor"] = round(floor / cold["gem"], 3)
                 # Cold (write scrub, the earlier method): a 512 MB scrub write before every
                 # call, each call timed alone with HIP events. The scrub leaves the MALL
                 # full of dirty lines that the call then writes back, and single-call event

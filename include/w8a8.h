@@ -239,6 +239,18 @@ int64_t w8a8_mfma_ceiling_ops(int64_t iters);
 w8a8_status w8a8_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int64_t N,
                               int64_t K, int64_t iters, uint32_t *wave_sums, void *stream);
 
+/* ---- Measurement aid (not part of the linear): the HBM read ceiling for a byte count.
+ * A weight-streaming GEMM with few tokens is bound by reading Wq once; the rate HBM
+ * delivers for a read of that size (with its ramp and drain) is below the datasheet's
+ * 8 TB/s, and this call measures it: a plain streaming read of `bytes` bytes at p
+ * (device memory, 16-byte aligned) by W8A8_READ_BLOCKS workgroups, workgroup b reading
+ * the b-th contiguous chunk of bytes / W8A8_READ_BLOCKS bytes and writing the XOR of its
+ * 32-bit words to sums[b] (uint32 [W8A8_READ_BLOCKS] on the device; a checksum, so the
+ * reads cannot be elided). bytes must be a positive multiple of 16 * W8A8_READ_BLOCKS
+ * (else W8A8_ERR_SHAPE); a misaligned p or sums returns W8A8_ERR_ARG. */
+#define W8A8_READ_BLOCKS 2048
+w8a8_status w8a8_read_ceiling(const void *p, int64_t bytes, uint32_t *sums, void *stream);
+
 /* Static description of a status code. */
 const char *w8a8_status_string(w8a8_status status);
 

@@ -32,7 +32,8 @@ __all__ = ["quantize_weight", "quantize_act", "gemm", "linear", "gemm_acc_i32",
            "col_absmax", "smooth_factors", "ACTS",
            "tile_count", "tile_name", "select_tile", "default_tile", "gemm_workspace_bytes",
            "linear_workspace_bytes", "linear_one_launch", "library_path", "load_library", "W8A8Error",
-           "MAX_K", "version", "mfma_ceiling", "mfma_ceiling_ops"]
+           "MAX_K", "version", "mfma_ceiling", "mfma_ceiling_ops", "read_ceiling",
+           "READ_BLOCKS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libw8a8.so")
@@ -87,6 +88,7 @@ def load_library():
         "w8a8_version": ([], ctypes.c_char_p),
         "w8a8_mfma_ceiling_ops": ([I64], I64),
         "w8a8_mfma_ceiling": ([P, P, I64, I64, I64, I64, P, P], INT),
+        "w8a8_read_ceiling": ([P, I64, P, P], INT),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -383,4 +385,25 @@ def mfma_ceiling(xq, wq, iters: int, *, out=None):
     with torch.cuda.device(xq.device):
         _call("w8a8_mfma_ceiling", _ptr(xq), _ptr(wq), M, N, K, int(iters), _ptr(sums),
               _stream(xq.device))
+    return sums
+
+
+READ_BLOCKS = 2048
+
+
+def read_ceiling(buf: torch.Tensor, *, out=None):
+    """Measurement aid: a plain streaming read of buf's bytes (contiguous, 16-byte
+    aligned, nbytes a multiple of 16 * READ_BLOCKS). Returns the per-workgroup XOR
+    checksums (int32 [READ_BLOCKS]); its launch time is the HBM read floor for that
+    many bytes."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    nbytes = buf.numel() * buf.element_size()
+    sums = out if out is not None else torch.empty(READ_BLOCKS, dtype=torch.int32,
+                                                   device=buf.device)
+    _check(sums, torch.int32, 1, "out")
+    if sums.numel() < READ_BLOCKS or sums.device != buf.device:
+        raise ValueError(f"out needs {READ_BLOCKS} entries on buf's device")
+    with torch.cuda.device(buf.device):
+        _call("w8a8_read_ceiling", _ptr(buf), nbytes, _ptr(sums), _stream(buf.device))
     return sums

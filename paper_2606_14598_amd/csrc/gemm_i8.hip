@@ -927,6 +927,250 @@ gemm_i8_skinny_kernel(KParams kp) {
     }
 }
 
+// LDS layout of the few-token kernel with the token block in LDS (gemm_i8_wsx_kernel):
+// token code rows of wsx_row_stride(K) bytes (= 16 mod 256: the 16 rows of a fragment
+// read fall in distinct banks), then with QX the bf16 rows of wsx_stage_stride(K)
+// bytes, 16 * fmb row scales, nw cross-wavefront maxima, and the reduction array of
+// nw x fnb x fmb x 1 KB.
+__host__ __device__ constexpr int wsx_row_stride(int K) { return (K + 1023) / 1024 * 1024 + 16; }
+__host__ __device__ constexpr int wsx_stage_stride(int K) { return (2 * K + 1023) / 1024 * 1024; }
+__host__ __device__ constexpr int wsx_red_offset(int rows, int K, bool qx, int fmb, int nw) {
+    return (rows * wsx_row_stride(K) + (qx ? rows * wsx_stage_stride(K) : 0) + 64 * fmb + 4 * nw +
+            15) / 16 * 16;
+}
+__host__ __device__ constexpr int64_t wsx_lds_bytes(int64_t rows, int64_t K, bool qx, int fmb,
+                                                    int fnb, int nw) {
+    return (rows * ((K + 1023) / 1024 * 1024 + 16) + (qx ? rows * ((2 * K + 1023) / 1024 * 1024) : 0) +
+            64 * fmb + 4 * nw + 15) / 16 * 16 + (int64_t)nw * fnb * fmb * 1024;
+}
+
+// Weight-streaming kernel with a register ring and the token block staged in LDS, for a
+// few tokens (M <= 16 * FMB per block). The product is bound by reading W once. A
+// workgroup owns 16 * FNB channels; its NW wavefronts split K in super-steps of 128
+// bytes (super-step j to wavefront j % NW) and keep D super-steps of their weight
+// fragments in flight in registers, loaded straight from global memory. Every
+// wavefront needs the whole token block, so the block goes to LDS once per workgroup:
+// its loads are issued first, by direct-to-LDS buffer loads, then the weight ring, and
+// the workgroup waits only for the token loads before it starts (the weight loads stay
+// in flight). With QX (the one-launch linear) the bf16 rows are staged instead and
+// quantized in LDS with the row quantizer's arithmetic while the weight loads are in
+// flight.
+//
+// v_mfma_i32_16x16x64_i8: lane (r, g) holds row r = lane % 16 of a fragment and 16
+// K-bytes; in super-step j it takes bytes [128 j + 64 s + 16 g, +16) for K-step s = 0, 1
+// (the same permutation of K for both operands leaves the dot product unchanged), so a
+// weight load reads 64 contiguous bytes of 16 rows. Weight rows past N and bytes past K
+// read as zero through the buffer descriptor. LDS rows of the token block are QS bytes
+// apart, QS = 16 (mod 256), so the 16 rows of a fragment read hit distinct banks. Partial
+// sums meet in LDS (integer, exact), then the epilogue runs.
+template <int FMB, int FNB, int NW, int D, int EPI, bool QX>
+__global__ void __launch_bounds__(NW * 64)
+gemm_i8_wsx_kernel(KParams kp) {
+    const GemmArgs &a = kp.a;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int r = lane & 15, g = lane >> 4;
+    const int64_t n0 = (int64_t)(blockIdx.x % kp.tiles_n) * (16 * FNB);
+    const int64_t mb = (int64_t)(blockIdx.x / kp.tiles_n) * (16 * FMB);
+    const int64_t M = a.M, N = a.N;
+    const int K = (int)a.K;
+    const int rows_w = (int)((N - n0) < 16 * FNB ? (N - n0) : 16 * FNB);
+    const int rows_x = (int)((M - mb) < 16 * FMB ? (M - mb) : 16 * FMB);
+    const int QS = wsx_row_stride(K);
+
+    // One dynamic LDS object (the compiler's tracking of direct-to-LDS loads stays
+    // exact): token rows, QX staging rows, QX scales, cross-wavefront maxima, and the
+    // reduction array (wsx_lds_layout).
+    extern __shared__ __attribute__((aligned(1024))) int8_t wsx_lds[];
+    const int SB = wsx_stage_stride(K);
+    int8_t *const xs = wsx_lds;                                   // rows_x x QS codes
+    int8_t *const stage = xs + rows_x * QS;                       // QX: bf16 rows
+    float *const qscale = reinterpret_cast<float *>(stage + (QX ? rows_x * SB : 0));
+    uint32_t *const pmax = reinterpret_cast<uint32_t *>(qscale + 16 * FMB);
+    i32x4 *const red = reinterpret_cast<i32x4 *>(
+        wsx_lds + wsx_red_offset(rows_x, K, QX, FMB, NW));
+
+    // Token block loads first: segment t (1 KB) of row t / SEG lands at its LDS row.
+    {
+        const int SEG = QX ? SB / 1024 : QS / 1024;           // 1 KB segments per row
+        const int rowbytes = QX ? 2 * K : K;
+        const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+            QX ? (void *)(kp.x + mb * K) : (void *)(a.xq + mb * K), (short)0,
+            rows_x * rowbytes, kRsrcWord3);
+        for (int t = wave; t < rows_x * SEG; t += NW) {
+            const int row = t / SEG, seg = t - row * SEG;
+            const int col = seg * 1024 + lane * 16;
+            const int off = col < rowbytes ? row * rowbytes + col : kOOB;
+            int8_t *dst = (QX ? stage + row * SB : xs + row * QS) + seg * 1024;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rx, (__attribute__((address_space(3))) void *)dst, 16, off, 0, 0, 0);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // The weight ring: super-step ss of this wavefront into slot `slot`.
+    constexpr uint32_t kFar = 1u << 30;
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.wq + n0 * K), (short)0, rows_w * K, kRsrcWord3);
+    uint32_t wrow[FNB];
+#pragma unroll
+    for (int c = 0; c < FNB; ++c)
+        wrow[c] = (c * 16 + r < rows_w) ? (uint32_t)((c * 16 + r) * K) : kFar;
+    const int nss = (K + 127) / 128;
+    const int mine = wave < nss ? (nss - wave + NW - 1) / NW : 0;
+    i32x4 wv[D][FNB][2];
+    auto load = [&](auto slotc, int ss) {
+        constexpr int slot = decltype(slotc)::value;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const int k = ss * 128 + s * 64 + g * 16;
+            const uint32_t kk = (uint32_t)k + ((uint32_t)((K - 1 - k) >> 31) & kFar);
+#pragma unroll
+            for (int c = 0; c < FNB; ++c)
+                wv[slot][c][s] = __builtin_bit_cast(
+                    i32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(wrow[c] + kk), 0, 0));
+        }
+    };
+    [&]<int... d>(std::integer_sequence<int, d...>) {
+        ((load(std::integral_constant<int, d>{}, wave + d * NW),
+          __builtin_amdgcn_sched_barrier(0)), ...);
+    }(std::make_integer_sequence<int, D>{});
+
+    // The token loads are older than the D * FNB * 2 weight loads of this wavefront.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(D * FNB * 2));
+    barrier_nofence();
+
+    if constexpr (QX) {
+        // Row i is quantized by WPR wavefronts (all NW share the rows evenly), each
+        // taking every WPR-th 16-byte vector of the row: absmax, cross-wavefront max,
+        // then the codes.
+        const int nvec = K >> 3;
+        int wpr = 1;                                 // a power of two, wpr * rows_x <= NW
+        while (2 * wpr * rows_x <= NW)
+            wpr *= 2;
+        const int part = wave % wpr, groups = NW / wpr;
+        const int rows_lim = (rows_x + groups - 1) / groups * groups;   // same trip count
+        for (int i0 = wave / wpr; i0 < rows_lim; i0 += groups) {
+            const bool live = i0 < rows_x;                     // wave-uniform
+            const uint4 *src = reinterpret_cast<const uint4 *>(stage + (live ? i0 : 0) * SB);
+            uint32_t mx = 0;
+            if (live)
+                for (int v = part * 64 + lane; v < nvec; v += wpr * 64)
+                    mx = max(mx, qmath::absmax8(src[v]));
+            mx = qmath::wave_max(mx);
+            if (lane == 0)
+                pmax[wave] = mx;
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            barrier_nofence();
+            if (live) {
+                uint32_t am = 0;
+                for (int w = 0; w < wpr; ++w)
+                    am = max(am, pmax[(wave / wpr) * wpr + w]);
+                const qmath::RowScale rs = qmath::row_scale(am);
+                for (int v = part * 64 + lane; v < nvec; v += wpr * 64)
+                    *reinterpret_cast<uint2 *>(xs + i0 * QS + v * 8) = qmath::code8(src[v], rs.inv);
+                if (part == 0 && lane == 0)
+                    qscale[i0] = rs.scale;
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            barrier_nofence();
+        }
+    }
+
+    i32x4 acc[FNB][FMB];
+#pragma unroll
+    for (int c = 0; c < FNB; ++c)
+#pragma unroll
+        for (int b = 0; b < FMB; ++b)
+            acc[c][b] = i32x4{0, 0, 0, 0};
+    // Token fragment rows past the block read row 0 and are zeroed.
+    int xrow[FMB];
+    bool xlive[FMB];
+#pragma unroll
+    for (int b = 0; b < FMB; ++b) {
+        xlive[b] = b * 16 + r < rows_x;
+        xrow[b] = (xlive[b] ? b * 16 + r : 0) * QS;
+    }
+    for (int it = 0; it < mine; it += D) {
+        [&]<int... d>(std::integer_sequence<int, d...>) {
+            ([&] {
+                const int ss = wave + (it + d) * NW;
+                __builtin_amdgcn_sched_barrier(0);
+                i32x4 xv[FMB][2];
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+#pragma unroll
+                    for (int b = 0; b < FMB; ++b) {
+                        const i32x4 t = *reinterpret_cast<const i32x4 *>(
+                            xs + xrow[b] + ss * 128 + s * 64 + g * 16);
+                        xv[b][s] = xlive[b] ? t : i32x4{0, 0, 0, 0};
+                    }
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+#pragma unroll
+                    for (int c = 0; c < FNB; ++c)
+#pragma unroll
+                        for (int b = 0; b < FMB; ++b)
+                            acc[c][b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                                wv[d][c][s], xv[b][s], acc[c][b], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                load(std::integral_constant<int, d>{}, ss + D * NW);
+            }(), ...);
+        }(std::make_integer_sequence<int, D>{});
+    }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+
+    // Cross-wavefront reduction: entry (wave, c * FMB + b) holds each lane's 4 sums.
+    constexpr int NCB = FNB * FMB;
+#pragma unroll
+    for (int c = 0; c < FNB; ++c)
+#pragma unroll
+        for (int b = 0; b < FMB; ++b)
+            red[(wave * NCB + c * FMB + b) * 64 + lane] = acc[c][b];
+    __syncthreads();
+    for (int cb = wave; cb < NCB; cb += NW) {
+        const int c = cb / FMB, b = cb % FMB;
+        i32x4 t = red[cb * 64 + lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w)
+            t += red[(w * NCB + cb) * 64 + lane];
+        const int64_t n = n0 + c * 16 + g * 4;
+        if (b * 16 + r >= rows_x || n >= N)
+            continue;
+        const int64_t m = mb + b * 16 + r;
+        if constexpr (EPI == EPI_I32) {
+            int32_t *o = static_cast<int32_t *>(a.out) + m * N + n;
+            if (kp.out_vec && n + 3 < N) {
+                *reinterpret_cast<i32x4 *>(o) = t;
+            } else {
+                for (int e = 0; e < 4 && n + e < N; ++e)
+                    o[e] = t[e];
+            }
+        } else {
+            uint16_t *o = static_cast<uint16_t *>(a.out) + m * N + n;
+            const float sxm = QX ? qscale[b * 16 + r] : a.sx[m];
+            uint16_t hv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (n + e < N) {
+                    const float bb = a.bias ? __uint_as_float((uint32_t)a.bias[n + e] << 16) : 0.0f;
+                    const float y = __builtin_fmaf((float)t[e], sxm * a.sw[n + e], bb);
+                    hv[e] = __builtin_bit_cast(uint16_t, (__bf16)y);
+                }
+            }
+            if (kp.out_vec && n + 3 < N) {
+                uint2 pk;
+                pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+                pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+                *reinterpret_cast<uint2 *>(o) = pk;
+            } else {
+                for (int e = 0; e < 4 && n + e < N; ++e)
+                    o[e] = hv[e];
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- tile registry
 
 // Split-K reduction and epilogue: acc = sum of the k_split int32 partials (exact in any
@@ -1037,6 +1281,41 @@ struct SkinnyTile {
     }
 };
 
+// Few tokens with the token block in LDS (the weight streamed through a register ring).
+// A token block too large for LDS runs the register-staged streaming kernel of the same
+// tile instead; the one-launch linear (kp.x set) is only chosen where it fits.
+template <int FMB, int FNB, int NW, int D>
+struct WsxTile {
+    static constexpr int threads = NW * 64;
+    template <int EPI, bool QX>
+    static hipError_t go(const KParams &kp, size_t dyn, hipStream_t s) {
+        static bool attr = false;   // dynamic LDS beyond the default limit, set once
+        if (!attr) {
+            (void)hipFuncSetAttribute(
+                reinterpret_cast<const void *>(&gemm_i8_wsx_kernel<FMB, FNB, NW, D, EPI, QX>),
+                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            attr = true;
+        }
+        hipLaunchKernelGGL((gemm_i8_wsx_kernel<FMB, FNB, NW, D, EPI, QX>),
+                           dim3((unsigned)(kp.tiles_m * kp.tiles_n)), dim3(threads), dyn, s, kp);
+        return hipGetLastError();
+    }
+    static hipError_t launch(Epilogue epi, const KParams &kp, hipStream_t s) {
+        const int64_t rows = kp.a.M < 16 * FMB ? kp.a.M : 16 * FMB;
+        const bool qx = kp.x != nullptr;
+        const int64_t dyn = wsx_lds_bytes(rows, kp.a.K, qx, FMB, FNB, NW);
+        if (dyn > 160 * 1024) {
+            if (qx)
+                return hipErrorInvalidValue;
+            return SkinnyTile<FMB, FNB, 16>::launch(epi, kp, s);
+        }
+        if (qx)
+            return go<EPI_BF16, true>(kp, (size_t)dyn, s);
+        return epi == EPI_BF16 ? go<EPI_BF16, false>(kp, (size_t)dyn, s)
+                               : go<EPI_I32, false>(kp, (size_t)dyn, s);
+    }
+};
+
 // Unaligned operands or K % 16 != 0: the register-staged kernel with byte loads.
 struct GenericTile {
     static constexpr int tm = 128, tn = 128;
@@ -1076,6 +1355,12 @@ struct TileEntry {
         {NAME, 16 * FMB, 16 * FNB, 256, SkinnyTile<FMB, FNB, NW>::threads,                  \
          SkinnyTile<FMB, FNB, NW>::lds, 1, -1, 1},                                           \
             1, &SkinnyTile<FMB, FNB, NW>::launch                                             \
+    }
+
+#define W8A8_WSX(NAME, FMB, FNB, NW, D)                                                     \
+    TileEntry {                                                                              \
+        {NAME, 16 * FMB, 16 * FNB, 128, WsxTile<FMB, FNB, NW, D>::threads, 0, 1, -1, 2},     \
+            1, &WsxTile<FMB, FNB, NW, D>::launch                                             \
     }
 
 // Names: m<TM>n<TN>k<BK>w<WM>x<WN>[s<S>]; skinny_m<Mmax>n<C>w<NW> = weight-streaming
@@ -1128,6 +1413,12 @@ const TileEntry kTiles[] = {
     // 96 x 256: exactly 256 workgroups at 333 (..384) tokens and N = 16384 (7% faster
     // there than 128 x 256 on 192).
     W8A8_TILE("m96n256k128w1x4s3", 96, 256, 128, 1, 4, 8, 3),
+    // Few tokens, token block in LDS, weight through a register ring:
+    // wsx_m<Mmax>n<C>w<NW>d<D>.
+    W8A8_WSX("wsx_m16n16w8d4", 1, 1, 8, 4),
+    W8A8_WSX("wsx_m16n32w8d4", 1, 2, 8, 4),
+    W8A8_WSX("wsx_m16n64w8d4", 1, 4, 8, 4),
+    W8A8_WSX("wsx_m32n32w8d2", 2, 2, 8, 2),
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -1176,9 +1467,11 @@ int fallback_tile(int64_t M, int64_t N, int64_t K) {
         if (tiles >= cus)
             return id;
     }
-    // Few tokens: stream the weight (one workgroup per 16 channels).
+    // Few tokens: stream the weight (one workgroup per 16 channels), with the token
+    // block in LDS up to 16 tokens; for a few tokens on a wide weight the deep-ring
+    // 64 x 64 tile streams it faster.
     if (M <= 16)
-        return N >= 256 * 64 ? 17 : 15;
+        return (M > 1 && N >= 16384) ? 23 : 36;
     if (M <= 32)
         return 16;
     if (M <= 64)
@@ -1245,6 +1538,19 @@ bool linear_small_shape(int64_t M, int64_t N, int64_t K) {
     if (!t.streaming)
         return false;
     const int64_t rows = M < t.tm ? M : t.tm;
+    const int64_t channel_blocks = (N + t.tn - 1) / t.tn;
+    if (t.streaming == 2) {
+        // Token block in LDS: its bf16 rows, codes and the reduction array must fit; the
+        // quantization overlaps the first weight loads, so its length is no concern.
+        // Every workgroup reads the block's bf16 rows: at most as many bytes as its
+        // weight rows (2 * rows <= channels), else the separate quantizer is cheaper
+        // (measured: 16 tokens on 16 channels at K = 2048 run 1.6x slower fused).
+        if (wsx_lds_bytes(rows, K, true, t.tm / 16, t.tn / 16, t.threads / 64) > kLdsPerWorkgroup)
+            return false;
+        if (2 * rows > t.tn)
+            return false;
+        return channel_blocks * M * K * 2 <= ((int64_t)16 << 20);
+    }
     const int64_t dyn = rows * (K + 16) + rows * 4;
     if (dyn > 48 * 1024 || dyn + t.lds_bytes > kLdsPerWorkgroup)
         return false;
@@ -1255,7 +1561,6 @@ bool linear_small_shape(int64_t M, int64_t N, int64_t K) {
     const int64_t nw = t.threads / 64;
     if ((K / 8 + 63) / 64 * ((rows + nw - 1) / nw) > 7)
         return false;
-    const int64_t channel_blocks = (N + t.tn - 1) / t.tn;
     return channel_blocks * M * K * 2 <= ((int64_t)16 << 20);
 }
 

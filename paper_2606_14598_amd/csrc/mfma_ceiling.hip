@@ -1,5 +1,8 @@
-// Matrix-core ceiling on given int8 operands (a measurement aid, not part of the
-// linear): the int8 MFMA's sustained rate depends on the operand bits, because the chip
+// Measurement aids, not part of the linear. The read ceiling (at the end of the file)
+// is a plain streaming read of a buffer: the rate HBM actually delivers for that many
+// bytes, the floor of a weight-streaming GEMM that reads them once.
+//
+// Matrix-core ceiling on given int8 operands: the int8 MFMA's sustained rate depends on the operand bits, because the chip
 // lowers its clock under the matrix cores' switching power. This kernel replays the
 // GEMM's per-K-step MFMA sequence of the 160x256 tile (each wavefront: 2 weight
 // fragments x 5 token fragments of v_mfma_i32_32x32x32_i8 per K-step) on fragments of
@@ -76,7 +79,43 @@ mfma_ceiling_kernel(const int8_t *__restrict__ xq, const int8_t *__restrict__ wq
         wave_sums[blockIdx.x * 4 + wave] = t;
 }
 
+// A plain streaming read: workgroup b XORs the 32-bit words of chunk b (bytes / 2048
+// contiguous bytes) into sums[b]; each thread keeps 8 16-byte loads in flight.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(256)
+read_ceiling_kernel(const u32x4 *__restrict__ p, int64_t per, uint32_t *__restrict__ sums) {
+    const u32x4 *q = p + (int64_t)blockIdx.x * per;
+    u32x4 a = {0, 0, 0, 0};
+    for (int64_t i = threadIdx.x; i < per; i += 256 * 8) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = (i + u * 256 < per) ? __builtin_nontemporal_load(q + i + u * 256)
+                                       : u32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            a ^= v[u];
+    }
+    uint32_t t = a.x ^ a.y ^ a.z ^ a.w;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        t ^= (uint32_t)__shfl_xor((int)t, off, 64);
+    __shared__ uint32_t part[4];
+    if ((threadIdx.x & 63) == 0)
+        part[threadIdx.x >> 6] = t;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        sums[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 }  // namespace
+
+hipError_t launch_read_ceiling(const void *p, int64_t bytes, uint32_t *sums, hipStream_t s) {
+    hipLaunchKernelGGL(read_ceiling_kernel, dim3(kReadBlocks), dim3(256), 0, s,
+                       static_cast<const u32x4 *>(p), bytes / 16 / kReadBlocks, sums);
+    return hipGetLastError();
+}
 
 int64_t mfma_ceiling_ops(int64_t iters) {
     return (int64_t)256 * 4 * iters * kSteps * kFN * kFM * (2 * 32 * 32 * 32);

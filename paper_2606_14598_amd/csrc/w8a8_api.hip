@@ -366,6 +366,16 @@ w8a8_status w8a8_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int
                                         as_stream(stream)));
 }
 
+w8a8_status w8a8_read_ceiling(const void *p, int64_t bytes, uint32_t *sums, void *stream) {
+    if (!p || !sums)
+        return W8A8_ERR_NULL;
+    if (bytes < 16 * kReadBlocks || bytes % (16 * kReadBlocks) != 0)
+        return W8A8_ERR_SHAPE;
+    if (!aligned16(p) || reinterpret_cast<uintptr_t>(sums) % 4 != 0)
+        return W8A8_ERR_ARG;
+    return from_hip(launch_read_ceiling(p, bytes, sums, as_stream(stream)));
+}
+
 const char *w8a8_version(void) { return "w8a8-gfx950 0.1.0"; }
 
 }  // extern "C"

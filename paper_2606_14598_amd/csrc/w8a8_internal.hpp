@@ -78,4 +78,9 @@ int64_t mfma_ceiling_ops(int64_t iters);
 hipError_t launch_mfma_ceiling(const int8_t *xq, const int8_t *wq, int64_t M, int64_t N,
                                int64_t K, int iters, uint32_t *wave_sums, hipStream_t s);
 
+// Plain streaming read of `bytes` bytes (a multiple of 16 * kReadBlocks) at p: workgroup
+// b of kReadBlocks XORs the 32-bit words of the b-th contiguous chunk into sums[b].
+constexpr int kReadBlocks = 2048;
+hipError_t launch_read_ceiling(const void *p, int64_t bytes, uint32_t *sums, hipStream_t s);
+
 }  // namespace w8a8

@@ -122,7 +122,7 @@ def sweep(iters: int, which: str = "all"):
         it = iters if s.ops < 5e14 else max(3, iters // 4)
         def wanted(t):
             name = w8a8.tile_name(t)
-            if s.M > 128 and name.startswith("skinny"):
+            if s.M > 128 and name.startswith(("skinny", "wsx")):
                 return False
             d = _tile_dims(name)
             # split-K only pays where the unsplit tiles leave CUs idle

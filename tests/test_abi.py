@@ -191,10 +191,10 @@ def test_default_tile_follows_the_wave_cost_model(lib):
             if cost is None or est < cost:
                 best, cost = i, est
         assert lib.w8a8_default_tile(M, N, K) == best, (M, N, K)
-    # few tokens: weight-streaming tiles
+    # few tokens: weight-streaming tiles (the token block in LDS up to 16 tokens)
     for M in (1, 16, 64, 128):
         name = lib.w8a8_tile_name(lib.w8a8_default_tile(M, 128, 4096)).decode()
-        assert name.startswith("skinny"), (M, name)
+        assert name.startswith("wsx" if M <= 16 else "skinny"), (M, name)
     assert lib.w8a8_default_tile(0, 8, 8) == -1
 
 
@@ -212,6 +212,18 @@ def test_mfma_ceiling_validation(lib):
     assert lib.w8a8_mfma_ceiling_ops(0) == -1
 
 
+def test_read_ceiling_validation(lib):
+    P = ctypes.c_void_p
+    fake = P(256)  # never dereferenced: validation fails first
+    unit = 16 * 2048
+    assert lib.w8a8_read_ceiling(None, unit, fake, None) == ERR_NULL
+    assert lib.w8a8_read_ceiling(fake, unit, None, None) == ERR_NULL
+    assert lib.w8a8_read_ceiling(fake, 0, fake, None) == ERR_SHAPE
+    assert lib.w8a8_read_ceiling(fake, unit + 16, fake, None) == ERR_SHAPE
+    assert lib.w8a8_read_ceiling(P(264), unit, fake, None) == ERR_ARG
+    assert lib.w8a8_read_ceiling(fake, unit, P(258), None) == ERR_ARG
+
+
 def _skinny_static_lds(name: str) -> int:
     """Static LDS of a weight-streaming tile, from its name skinny_m<M>n<C>w<NW>: the
     cross-wavefront reduction array holds NW x (C/16) x (M/16) x 64 lanes x 16 bytes."""
@@ -221,24 +233,48 @@ def _skinny_static_lds(name: str) -> int:
     return nw * (tn // 16) * (tm // 16) * 64 * 16
 
 
+def _wsx_lds(name: str, rows: int, K: int) -> int:
+    """LDS of the one-launch linear on a token-block-in-LDS tile wsx_m<M>n<C>w<NW>d<D>:
+    code rows of ceil(K / 1024) KiB + 16 bytes, bf16 rows of ceil(2K / 1024) KiB, M/16 x
+    16 scales and NW maxima (4 bytes each) rounded up to 16 bytes, and the reduction
+    array of NW x (C/16) x (M/16) x 1 KiB."""
+    m = re.match(r"wsx_m(\d+)n(\d+)w(\d+)d(\d+)$", name)
+    assert m, name
+    tm, tn, nw, _ = (int(g) for g in m.groups())
+    head = rows * (-(-K // 1024) * 1024 + 16) + rows * (-(-2 * K // 1024) * 1024)
+    head += 4 * tm + 4 * nw
+    head = -(-head // 16) * 16
+    return head + nw * (tn // 16) * (tm // 16) * 1024
+
+
 def test_one_launch_linear_fits_the_workgroup_lds(lib):
-    """Wherever w8a8_linear takes the one-launch path, the token block's codes (rows of
-    K + 16 bytes) and scales plus the tile's static LDS fit gfx950's 160 KiB."""
+    """Wherever w8a8_linear takes the one-launch path, the tile's LDS fits gfx950's
+    160 KiB: on the register-staged streaming tiles the token block's codes (rows of
+    K + 16 bytes) and scales plus the static reduction array; on the tiles that keep
+    the token block in LDS, the whole layout of bf16 rows, codes and reduction array."""
     budget = 160 * 1024
-    seen = 0
+    seen = {"skinny": 0, "wsx": 0}
     for M in list(range(1, 129)):
-        for K in (16, 256, 512, 768, 1024, 2048, 3136, 4096):
+        for K in (16, 256, 512, 768, 1024, 2048, 3136, 4096, 8192, 16384):
             for N in (64, 520, 4096, 16384):
                 if not lib.w8a8_linear_one_launch(M, N, K):
                     continue
-                seen += 1
                 name = lib.w8a8_tile_name(lib.w8a8_select_tile(M, N, K)).decode()
+                if name.startswith("wsx"):
+                    seen["wsx"] += 1
+                    tm = int(re.match(r"wsx_m(\d+)", name).group(1))
+                    assert _wsx_lds(name, min(M, tm), K) <= budget, (M, N, K, name)
+                    continue
+                seen["skinny"] += 1
                 tm = int(re.match(r"skinny_m(\d+)", name).group(1))
                 rows = min(M, tm)
                 dyn = rows * (K + 16) + rows * 4
                 assert dyn <= 48 * 1024, (M, N, K, name)
                 assert dyn + _skinny_static_lds(name) <= budget, (M, N, K, name)
-    assert seen > 100
+    assert seen["skinny"] > 50 and seen["wsx"] > 50, seen
+    # a token block too large for LDS does not take the one-launch path
+    assert not lib.w8a8_linear_one_launch(16, 64, 16384)
+    assert lib.w8a8_linear_one_launch(1, 4096, 16384)
     # shapes that once passed the dynamic check alone but overflow the total
     assert not lib.w8a8_linear_one_launch(64, 4096, 512)
     assert not lib.w8a8_linear_one_launch(48, 4096, 768)

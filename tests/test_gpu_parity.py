@@ -178,7 +178,7 @@ def _acc_case(M, N, K, seed):
 
 
 # The library's tile count; test_tile_count_matches keeps it honest.
-NUM_TILES = 36
+NUM_TILES = 40
 
 
 def test_tile_count_matches():
@@ -445,17 +445,36 @@ def test_mfma_ceiling_checksums(M, N, K):
         assert np.array_equal(got, (iters * base) % (1 << 32)), iters
 
 
+@pytest.mark.parametrize("nbytes", [16 * 2048, 16 * 2048 * 37, 4096 * 4096])
+def test_read_ceiling_checksums(nbytes):
+    """The read-ceiling probe reads every byte it is given: workgroup b's checksum is the
+    XOR of the 32-bit words of the b-th contiguous chunk."""
+    say(f"read ceiling {nbytes} bytes")
+    rng = np.random.default_rng(nbytes)
+    words = rng.integers(0, 1 << 32, size=nbytes // 4, dtype=np.uint64).astype(np.uint32)
+    sums = host(w8a8.read_ceiling(torch.from_numpy(words.view(np.int32)).cuda()))
+    want = np.bitwise_xor.reduce(words.reshape(w8a8.READ_BLOCKS, -1), axis=1)
+    assert np.array_equal(sums.view(np.uint32), want)
+
+
 # ---------------------------------------------------------------- small fused linear
 
 # (M, K, N, fused): few tokens whose tile streams the weight run quantizer and GEMM in
 # one launch (the workspace stays untouched); the rest keep the two-launch path: a tile
-# that does not stream the weight (M = 1, N = 16384 picks a tiled kernel; M = 77, 2560),
-# a token block over the LDS budget (13 x 4112), more than 7 vectors per lane to
-# quantize (K = 4096), K % 16 != 0 (264).
-SMALL_FUSED = [(64, 256, 128, True), (1, 4096, 4096, False), (1, 4096, 16384, False),
-               (1, 3136, 4096, True), (5, 1024, 520, True), (16, 2048, 4096, True),
-               (13, 3088, 80, True), (13, 4112, 80, False), (77, 3136, 4096, False),
-               (2560, 256, 64, False), (3, 264, 64, False),
+# that does not stream the weight (M = 77, 2560; M = 4, N = 16384), a token block over
+# the LDS budget (64 x 4112 on the register-staged streaming tiles), more than 7
+# vectors per lane to quantize there (M = 64, K = 4096), more bf16 token bytes than
+# weight bytes per workgroup on the token-block-in-LDS tiles (13 or 16 tokens on 16
+# channels), K % 16 != 0 (264). Up to 8 tokens the token block sits in LDS: one row
+# quantized by 8, 4 or 2 wavefronts (M = 1, 2, 3), one per wavefront (7, 8), with K
+# tails (528, 3088) and ragged channel blocks (300, 520).
+SMALL_FUSED = [(64, 256, 128, True), (1, 4096, 4096, True), (1, 4096, 16384, True),
+               (1, 3136, 4096, True), (5, 1024, 520, True), (16, 2048, 4096, False),
+               (4, 4096, 16384, False), (8, 3088, 80, True), (13, 3088, 80, False),
+               (64, 4112, 80, False), (77, 3136, 4096, False),
+               (2560, 256, 64, False), (3, 264, 64, False), (2, 16, 40, True),
+               (3, 528, 300, True), (7, 4096, 64, True), (16, 1024, 48, False),
+               (64, 4096, 128, False), (1, 16384, 4096, True),
                # codes + scales fit 48 KB but not beside the tile's 128 KB reduction array
                (64, 512, 4096, False), (48, 768, 4096, False)]
 
