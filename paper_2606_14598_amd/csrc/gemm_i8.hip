@@ -931,20 +931,22 @@ gemm_i8_skinny_kernel(KParams kp) {
 }
 
 // LDS layout of the few-token kernel with the token block in LDS (gemm_i8_wsx_kernel):
-// token code rows of wsx_row_stride(K) bytes (= 16 mod 256: the 16 rows of a fragment
-// read fall in distinct banks), then with QX the bf16 rows of wsx_stage_stride(K)
-// bytes, 16 * fmb row scales, nw cross-wavefront maxima, and the reduction array of
-// nw x fnb x fmb x 1 KB.
+// a head of 16 * fmb row scales and nw cross-wavefront maxima (256-byte aligned), then
+// the token code rows of wsx_row_stride(K) bytes (= 16 mod 256: the 16 rows of a
+// fragment read fall in distinct banks) and, with QX, the bf16 rows of
+// wsx_stage_stride(K) bytes. After the main loop the reduction array (nw x fnb x fmb x
+// 1 KB) takes the place of the rows, so the object holds the larger of the two.
 __host__ __device__ constexpr int wsx_row_stride(int K) { return (K + 1023) / 1024 * 1024 + 16; }
 __host__ __device__ constexpr int wsx_stage_stride(int K) { return (2 * K + 1023) / 1024 * 1024; }
-__host__ __device__ constexpr int wsx_red_offset(int rows, int K, bool qx, int fmb, int nw) {
-    return (rows * wsx_row_stride(K) + (qx ? rows * wsx_stage_stride(K) : 0) + 64 * fmb + 4 * nw +
-            15) / 16 * 16;
+__host__ __device__ constexpr int wsx_head_bytes(int fmb, int nw) {
+    return (64 * fmb + 4 * nw + 255) / 256 * 256;
 }
 __host__ __device__ constexpr int64_t wsx_lds_bytes(int64_t rows, int64_t K, bool qx, int fmb,
                                                     int fnb, int nw) {
-    return (rows * ((K + 1023) / 1024 * 1024 + 16) + (qx ? rows * ((2 * K + 1023) / 1024 * 1024) : 0) +
-            64 * fmb + 4 * nw + 15) / 16 * 16 + (int64_t)nw * fnb * fmb * 1024;
+    const int64_t body = rows * ((K + 1023) / 1024 * 1024 + 16) +
+                         (qx ? rows * ((2 * K + 1023) / 1024 * 1024) : 0);
+    const int64_t red = (int64_t)nw * fnb * fmb * 1024;
+    return wsx_head_bytes(fmb, nw) + (body > red ? body : red);
 }
 
 // Weight-streaming kernel with a register ring and the token block staged in LDS, for a
@@ -982,16 +984,16 @@ gemm_i8_wsx_kernel(KParams kp) {
     const int QS = wsx_row_stride(K);
 
     // One dynamic LDS object (the compiler's tracking of direct-to-LDS loads stays
-    // exact): token rows, QX staging rows, QX scales, cross-wavefront maxima, and the
-    // reduction array (wsx_lds_layout).
+    // exact), laid out as wsx_lds_bytes describes: QX scales and cross-wavefront maxima,
+    // then the token rows and QX staging rows, whose place the reduction array takes
+    // after the main loop.
     extern __shared__ __attribute__((aligned(1024))) int8_t wsx_lds[];
     const int SB = wsx_stage_stride(K);
-    int8_t *const xs = wsx_lds;                                   // rows_x x QS codes
-    int8_t *const stage = xs + rows_x * QS;                       // QX: bf16 rows
-    float *const qscale = reinterpret_cast<float *>(stage + (QX ? rows_x * SB : 0));
+    float *const qscale = reinterpret_cast<float *>(wsx_lds);
     uint32_t *const pmax = reinterpret_cast<uint32_t *>(qscale + 16 * FMB);
-    i32x4 *const red = reinterpret_cast<i32x4 *>(
-        wsx_lds + wsx_red_offset(rows_x, K, QX, FMB, NW));
+    int8_t *const xs = wsx_lds + wsx_head_bytes(FMB, NW);         // rows_x x QS codes
+    int8_t *const stage = xs + rows_x * QS;                       // QX: bf16 rows
+    i32x4 *const red = reinterpret_cast<i32x4 *>(xs);
 
     // Token block loads first: segment t (1 KB) of row t / SEG lands at its LDS row.
     {
@@ -1122,6 +1124,9 @@ gemm_i8_wsx_kernel(KParams kp) {
         }(std::make_integer_sequence<int, D>{});
     }
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    // The reduction array overwrites the token rows: every wavefront's reads of them
+    // have to be done first.
+    __syncthreads();
 
     // Cross-wavefront reduction: entry (wave, c * FMB + b) holds each lane's 4 sums.
     constexpr int NCB = FNB * FMB;
@@ -1442,7 +1447,8 @@ static_assert(sizeof(kTileCost) / sizeof(kTileCost[0]) == kNumTiles, "one cost p
 // Shapes without a table entry. Above 128 tokens a wave-quantization cost model picks
 // the tile: a launch of T workgroups on 256 CUs takes ceil(T / 256) rounds, and a round
 // of tile t costs c_t + d_t * K * TM * TN / 1e9 (kTileCost, fitted offline to the
-// sweep). With few tokens the weight-streaming kernels take over.
+// sweep). With few tokens, rules from a sweep of the weight-streaming and deep-ring
+// tiles pick it.
 int fallback_tile(int64_t M, int64_t N, int64_t K) {
     const int64_t cus = 256;
     if (M > 128) {
@@ -1464,24 +1470,23 @@ int fallback_tile(int64_t M, int64_t N, int64_t K) {
         if (best >= 0)
             return best;
     }
-    for (int id : {0, 2, 3, 4, 12}) {
-        const TileInfo &t = kTiles[id].info;
-        const int64_t tiles = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
-        if (tiles >= cus)
-            return id;
-    }
-    // Few tokens: stream the weight (one workgroup per 16 channels), with the token
-    // block in LDS up to 16 tokens; for a few tokens on a wide weight the deep-ring
-    // 64 x 64 tile streams it faster.
+    // Few tokens (a sweep of the streaming and deep-ring tiles over M = 2..128,
+    // N = 1024..16384, K = 1024..16384). Up to 16 tokens: the token block in LDS, except
+    // for 2-16 tokens on a wide weight, where the deep-ring 64 x 64 tile streams it faster.
     if (M <= 16)
         return (M > 1 && N >= 16384) ? 23 : 36;
+    // Few channels: the token block in LDS on 16 (32) channels per workgroup.
+    if (N <= 2048)
+        return M <= 64 ? 36 : 37;
+    // A long K on a few thousand channels: the deep-ring tiles with K split in four.
+    if (K >= 8192 && N < 8192)
+        return M <= 64 ? 29 : 28;
+    // Many channels: the deep-ring tiles fill the CUs.
+    if (N >= 8192)
+        return M <= 64 ? 22 : 21;
     if (M <= 32)
         return 16;
-    if (M <= 64)
-        return 18;
-    if (M <= 128)
-        return 19;
-    return 12;
+    return M <= 64 ? 39 : 23;
 }
 
 }  // namespace

@@ -191,10 +191,17 @@ def test_default_tile_follows_the_wave_cost_model(lib):
             if cost is None or est < cost:
                 best, cost = i, est
         assert lib.w8a8_default_tile(M, N, K) == best, (M, N, K)
-    # few tokens: weight-streaming tiles (the token block in LDS up to 16 tokens)
-    for M in (1, 16, 64, 128):
-        name = lib.w8a8_tile_name(lib.w8a8_default_tile(M, 128, 4096)).decode()
-        assert name.startswith("wsx" if M <= 16 else "skinny"), (M, name)
+    # few tokens: the swept rules (M, N, K) -> tile
+    rules = {(1, 128, 4096): "wsx_m16n16w8d4", (16, 4096, 4096): "wsx_m16n16w8d4",
+             (8, 16384, 4096): "m64n64k128w2x2s8", (1, 16384, 4096): "wsx_m16n16w8d4",
+             (64, 128, 4096): "wsx_m16n16w8d4", (128, 2048, 4096): "wsx_m16n32w8d4",
+             (40, 4096, 16384): "m32n128k128w1x4s6_k4", (100, 4096, 8192): "m64n128k128w1x4s6_k4",
+             (40, 16384, 4096): "m32n128k128w1x4s6", (128, 8192, 4096): "m64n128k128w1x4s6",
+             (17, 4096, 4096): "skinny_m32n16w16", (32, 3072, 1024): "skinny_m32n16w16",
+             (33, 4096, 4096): "wsx_m32n32w8d2", (64, 4096, 1024): "wsx_m32n32w8d2",
+             (65, 4096, 4096): "m64n64k128w2x2s8", (128, 4096, 2048): "m64n64k128w2x2s8"}
+    for (M, N, K), want in rules.items():
+        assert lib.w8a8_tile_name(lib.w8a8_default_tile(M, N, K)).decode() == want, (M, N, K)
     assert lib.w8a8_default_tile(0, 8, 8) == -1
 
 
@@ -235,16 +242,16 @@ def _skinny_static_lds(name: str) -> int:
 
 def _wsx_lds(name: str, rows: int, K: int) -> int:
     """LDS of the one-launch linear on a token-block-in-LDS tile wsx_m<M>n<C>w<NW>d<D>:
-    code rows of ceil(K / 1024) KiB + 16 bytes, bf16 rows of ceil(2K / 1024) KiB, M/16 x
-    16 scales and NW maxima (4 bytes each) rounded up to 16 bytes, and the reduction
-    array of NW x (C/16) x (M/16) x 1 KiB."""
+    M/16 x 16 scales and NW maxima (4 bytes each) rounded up to 256 bytes, then the
+    larger of (code rows of ceil(K / 1024) KiB + 16 bytes and bf16 rows of
+    ceil(2K / 1024) KiB) and the reduction array of NW x (C/16) x (M/16) x 1 KiB, which
+    reuses the rows' space once the main loop is done."""
     m = re.match(r"wsx_m(\d+)n(\d+)w(\d+)d(\d+)$", name)
     assert m, name
     tm, tn, nw, _ = (int(g) for g in m.groups())
-    head = rows * (-(-K // 1024) * 1024 + 16) + rows * (-(-2 * K // 1024) * 1024)
-    head += 4 * tm + 4 * nw
-    head = -(-head // 16) * 16
-    return head + nw * (tn // 16) * (tm // 16) * 1024
+    rows_bytes = rows * (-(-K // 1024) * 1024 + 16) + rows * (-(-2 * K // 1024) * 1024)
+    head = -(-(4 * tm + 4 * nw) // 256) * 256
+    return head + max(rows_bytes, nw * (tn // 16) * (tm // 16) * 1024)
 
 
 def test_one_launch_linear_fits_the_workgroup_lds(lib):

@@ -475,8 +475,13 @@ SMALL_FUSED = [(64, 256, 128, True), (1, 4096, 4096, True), (1, 4096, 16384, Tru
                (2560, 256, 64, False), (3, 264, 64, False), (2, 16, 40, True),
                (3, 528, 300, True), (7, 4096, 64, True), (16, 1024, 48, False),
                (64, 4096, 128, False), (1, 16384, 4096, True),
-               # codes + scales fit 48 KB but not beside the tile's 128 KB reduction array
-               (64, 512, 4096, False), (48, 768, 4096, False)]
+               # codes + scales fit 48 KB, yet not one launch (they once overflowed LDS
+               # beside a 128 KB reduction array)
+               (64, 512, 4096, False), (48, 768, 4096, False),
+               # the swept few-token rules: register-staged streaming tile, token block in
+               # LDS over several token blocks
+               (32, 512, 4096, True), (24, 4096, 4096, False), (100, 1024, 520, True),
+               (80, 512, 2048, True), (128, 3136, 520, False)]
 
 
 @pytest.mark.parametrize("M,K,N,fused", SMALL_FUSED)
