@@ -22,9 +22,10 @@
 //   * gemm_i8_skinny_kernel: few tokens (M <= 128). A workgroup streams 16*FNB weight
 //     rows once for all tokens with v_mfma_i32_16x16x64_i8, its wavefronts splitting K,
 //     partial sums reduced in LDS.
-//   * gemm_i8_wsx_kernel: up to 16 tokens. The same product with the token block staged
-//     once per workgroup in LDS and the weight streamed through a register ring; it
-//     also quantizes the bf16 token rows itself for the one-launch linear.
+//   * gemm_i8_wsx_kernel: few tokens, in blocks of 16 or 32. The same product with the
+//     token block staged once per workgroup in LDS and the weight streamed through a
+//     register ring; it also quantizes the bf16 token rows itself for the one-launch
+//     linear.
 // Workgroup ids are remapped so that each XCD (which receives every 8th id) owns a
 // contiguous run of tiles, traversed in groups of GM token-tiles: the operand panels a
 // run touches stay in that XCD's L2. The integer accumulation is exact, so every tile,
