@@ -238,7 +238,9 @@ def test_acc_against_torch_int_mm():
 
 LINEAR_SMALL = [(64, 256, 128, "outlier"), (257, 384, 391, "student_t"),
                 (130, 3136, 260, "gelu"), (1, 4096, 130, "outlier"), (77, 264, 64, "outlier"),
-                (45, 269, 77, "student_t"), (300, 512, 200, "outlier")]
+                (45, 269, 77, "student_t"), (300, 512, 200, "outlier"),
+                # few tokens on a long K: the fallback splits K in four inside w8a8_linear
+                (40, 8192, 4096, "student_t"), (100, 8192, 3072, "outlier")]
 
 
 @pytest.mark.parametrize("M,K,N,dist", LINEAR_SMALL)
