@@ -527,3 +527,42 @@ def test_small_fused_linear_zero_and_tiny_rows():
     assert sx_o[0] == 0 and sx_o[1] == 0
     assert np.array_equal(host_bits(y)[:2], np.stack([b, b]))
     assert_bf16_parity(host_bits(y), y_o, "fused zero/tiny rows")
+
+
+# ---------------------------------------------------------------- seeded random shapes
+
+def _random_shapes(n=24, seed=20261202):
+    """Shapes across the default tile rules: few tokens (the token-block and streaming
+    kernels, the deep-ring tiles, split-K on long K), a few hundred and more tokens
+    (the cost model), aligned and unaligned K. A fixed seed: the same shapes every run."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        M = int(rng.choice([1, 2, 5, 13, 16, 17, 31, 40, 64, 77, 100, 128, 129, 200, 333, 517]))
+        N = int(rng.integers(1, 5200)) if i % 3 else int(rng.choice([1024, 2048, 4096, 8192]))
+        K = int(rng.choice([16, 48, 272, 1040, 2048, 3136, 4096, 8192]))
+        if i % 5 == 4:
+            K += 8                                       # K % 16 != 0: the generic path
+        while M * N * K > 1_500_000_000:
+            N = max(1, N // 2)
+        out.append((M, K, N))
+    return out
+
+
+@pytest.mark.parametrize("M,K,N", _random_shapes())
+def test_random_shapes_against_oracle(M, K, N):
+    """w8a8_linear on the default tile of each shape against the oracle's linear: codes
+    and scales exact, the int32 accumulator exact through the debug path, the bf16
+    output within the bf16 gate."""
+    say(f"random shape M={M} K={K} N={N} tile={w8a8.tile_name(w8a8.select_tile(M, N, K))}")
+    x, w, b = si.make_inputs((M, K, N), seed=M * 31 + K * 7 + N, dist="student_t")
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, xq_o, sx_o, acc_o = oracle.linear(x, wq_o, sw_o, b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    assert np.array_equal(host(wq), wq_o) and np.array_equal(host(sw), sw_o)
+    y = w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b))
+    assert_bf16_parity(host_bits(y), y_o, f"random {M}x{K}x{N}")
+    xq, sx = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(xq), xq_o) and np.array_equal(host(sx), sx_o)
+    acc = w8a8.gemm_acc_i32(xq, wq)
+    assert np.array_equal(host(acc), acc_o)
