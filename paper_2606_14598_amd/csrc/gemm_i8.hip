@@ -33,6 +33,7 @@
 #include "w8a8_internal.hpp"
 #include "quant_math.hpp"
 
+#include <atomic>
 #include <utility>
 
 namespace w8a8 {
@@ -1298,12 +1299,22 @@ struct WsxTile {
     static constexpr int threads = NW * 64;
     template <int EPI, bool QX>
     static hipError_t go(const KParams &kp, size_t dyn, hipStream_t s) {
-        static bool attr = false;   // dynamic LDS beyond the default limit, set once
-        if (!attr) {
-            (void)hipFuncSetAttribute(
+        // Dynamic LDS beyond the default limit: a property of the kernel on each device,
+        // set on a device's first launch (one bit per device; setting it twice from
+        // racing threads is harmless).
+        static std::atomic<uint64_t> attr_set{0};
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess)
+            return e;
+        const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+        if (bit == 0 || (attr_set.load(std::memory_order_relaxed) & bit) == 0) {
+            e = hipFuncSetAttribute(
                 reinterpret_cast<const void *>(&gemm_i8_wsx_kernel<FMB, FNB, NW, D, EPI, QX>),
                 hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-            attr = true;
+            if (e != hipSuccess)
+                return e;
+            attr_set.fetch_or(bit, std::memory_order_relaxed);
         }
         hipLaunchKernelGGL((gemm_i8_wsx_kernel<FMB, FNB, NW, D, EPI, QX>),
                            dim3((unsigned)(kp.tiles_m * kp.tiles_n)), dim3(threads), dyn, s, kp);
