@@ -566,3 +566,23 @@ def test_random_shapes_against_oracle(M, K, N):
     assert np.array_equal(host(xq), xq_o) and np.array_equal(host(sx), sx_o)
     acc = w8a8.gemm_acc_i32(xq, wq)
     assert np.array_equal(host(acc), acc_o)
+
+
+EXTREME_SHAPES = [(1, 4096, 40000), (65536, 64, 40), (3, 133136, 8), (2, 133136, 300),
+                  (70000, 16, 1)]
+
+
+@pytest.mark.parametrize("M,K,N", EXTREME_SHAPES)
+def test_extreme_aspect_shapes_against_oracle(M, K, N):
+    """A wide weight at one token (2500 workgroups), many tokens on a tiny weight, K near
+    its maximum on tiny M and N: every output against the oracle's linear."""
+    say(f"extreme shape M={M} K={K} N={N} tile={w8a8.tile_name(w8a8.select_tile(M, N, K))}")
+    x, w, b = si.make_inputs((M, K, N), seed=M + 3 * K + 7 * N, dist="outlier")
+    wq_o, sw_o = oracle.quantize_rows(w)
+    y_o, xq_o, sx_o, acc_o = oracle.linear(x, wq_o, sw_o, b)
+    wq, sw = w8a8.quantize_weight(dev_bf16(w))
+    assert np.array_equal(host(wq), wq_o) and np.array_equal(host(sw), sw_o)
+    y = w8a8.linear(dev_bf16(x), wq, sw, dev_bf16(b))
+    assert_bf16_parity(host_bits(y), y_o, f"extreme {M}x{K}x{N}")
+    xq, sx = w8a8.quantize_act(dev_bf16(x))
+    assert np.array_equal(host(w8a8.gemm_acc_i32(xq, wq)), acc_o)
